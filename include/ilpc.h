@@ -1,0 +1,192 @@
+/*
+ * ilpc.h -- C ABI of the prefix-cached paged prefill attention library
+ * (libilpc.so) for AMD Instinct MI355X (gfx950).
+ *
+ * The operations are the hot path of LLM-based online log parsing with
+ * prefix caching, as described by InferLog (arXiv 2507.08523):
+ *   - a prompt is an instruction, k demonstrations and the queried log
+ *     (section 2.1.1, prompt format);
+ *   - KV of a shared prompt prefix is reused across requests at block
+ *     granularity, and a block is reusable only if every block before it is
+ *     reused too (section 2.1.2, "KV Cache and Prefix Caching", and its
+ *     three-request figure);
+ *   - the KV of cache-missing tokens is computed and stored (section 3.2.2);
+ *   - prefill over the uncached suffix against cached + new KV dominates the
+ *     latency (section 2.2.1).
+ *
+ * Conventions for every call:
+ *   - Return value: ILPC_OK (0) or a negative ILPC_E* code.  No exception or
+ *     abort crosses the ABI.  ilpc_last_error() gives a message for the last
+ *     failing call on the calling thread.
+ *   - Arguments are validated before any state change or kernel launch.  A
+ *     failing call leaves the cache unchanged; its outputs are unspecified.
+ *   - Host pointers are marked [host], device pointers [device].  The caller
+ *     owns every buffer; the library owns only the cache handle (host memory)
+ *     and allocates no device memory.
+ *   - bf16 tensors are passed as uint16_t* holding the raw bf16 bits.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Device calls are
+ *     asynchronous on that stream; they return ILPC_EHIP when the launch
+ *     fails.  Work ordered on one stream needs no other synchronisation.
+ *   - Supported shapes: block_size == 16, head_dim in {64, 128},
+ *     Hq % Hkv == 0, 1 <= Hq / Hkv <= 64.  Anything else is ILPC_EUNSUP.
+ *
+ * Device layouts (row-major, bf16):
+ *   k_pool [num_blocks, Hkv, 16, D]  key rows of a block, token-major
+ *   v_pool [num_blocks, Hkv, D, 16]  value rows of a block, transposed
+ *                                    (dimension-major), the operand layout
+ *                                    the matrix cores consume directly
+ *   q, out [total_q, Hq, D]          packed query / output rows
+ *   k_new, v_new [total_new, Hkv, D] packed rows to append
+ *   block_tables [B, max_blocks] int32, physical block of each logical
+ *                                    block of a request, -1 past the end
+ */
+#ifndef ILPC_H
+#define ILPC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ILPC_OK = 0,
+  ILPC_EINVAL = -1, /* bad argument (null pointer, negative size, bad lengths) */
+  ILPC_ENOSPC = -2, /* the block pool cannot hold the batch's new blocks */
+  ILPC_ETABLE = -3, /* the block-key table cannot hold the batch's new keys */
+  ILPC_EUNSUP = -4, /* shape outside the supported set */
+  ILPC_EHIP = -5    /* a HIP runtime call or kernel launch failed */
+};
+
+/* ilpc_prefix_match flags */
+#define ILPC_NO_LOOKUP 1u   /* ignore the table: every request has P = 0 */
+#define ILPC_NO_REGISTER 2u /* do not register the batch's new full blocks */
+
+typedef struct ilpc_cache ilpc_cache; /* opaque, host memory, library-owned */
+
+/* Message describing the last non-OK return on this thread ("" if none).
+ * The pointer stays valid until the next failing call on the same thread. */
+const char* ilpc_last_error(void);
+
+/* Create an empty prefix cache over a pool of `num_blocks` physical blocks of
+ * `block_size` tokens (must be 16).  The block-key table has
+ * 2^table_log2_cap slots (1 <= table_log2_cap <= 30) and holds at most
+ * 7/8 of that many keys.  *out receives the handle. */
+int ilpc_cache_create(int32_t num_blocks, int32_t block_size, int32_t table_log2_cap,
+                      ilpc_cache** out);
+
+/* Free a cache (NULL is ignored). */
+void ilpc_cache_destroy(ilpc_cache* cache);
+
+/* Forget every registered block and restart the block allocator at 0. */
+int ilpc_cache_reset(ilpc_cache* cache);
+
+/* stats[0] = registered keys, stats[1] = next free block id,
+ * stats[2] = key capacity (7/8 of the slots), stats[3] = num_blocks. */
+int ilpc_cache_stats(const ilpc_cache* cache, int64_t stats[4]);
+
+/* Record the current state so that ilpc_cache_rollback can return to it:
+ * mark[0] = registered-key journal length, mark[1] = next free block id. */
+int ilpc_cache_checkpoint(const ilpc_cache* cache, int64_t mark[2]);
+
+/* Undo every registration and block allocation made since `mark` was taken
+ * (most recent first).  A mark from before a later reset or rollback past it
+ * is rejected with ILPC_EINVAL. */
+int ilpc_cache_rollback(ilpc_cache* cache, const int64_t mark[2]);
+
+/*
+ * Block-level prefix matching of one batch (section 2.1.2).
+ *
+ * tokens      [host] int32 [cu_seqlens[B]]  the prompts, packed
+ * cu_seqlens  [host] int32 [B+1]            prompt r is tokens[cu[r]..cu[r+1]),
+ *                                           cu[0] = 0, every length >= 1
+ * B           number of prompts (0 is a no-op)
+ * reserve     [host] int32 [B] or NULL      extra tokens (later decode steps)
+ *                                           to allocate blocks for
+ * max_blocks  row length of block_tables; must be >= ceil((L_r+reserve_r)/16)
+ * flags       ILPC_NO_LOOKUP | ILPC_NO_REGISTER
+ * cached_len  [host] int32 [B]              out: P_r, a multiple of 16
+ * block_tables [host] int32 [B*max_blocks]  out: physical block ids, -1 pad
+ * block_keys  [host] uint64 [B*max_blocks] or NULL  out: chained key of each
+ *                                           full block, 0 past them
+ *
+ * Every full 16-token block b of prompt r gets the chained key
+ *   c_b = fmix64(c_{b-1} XOR d_b),  c_{-1} = 0x243F6A8885A308D3,
+ *   d_b = fmix64(sum_i fmix64(w_i XOR (i+1)*0x9E3779B97F4A7C15)), i = 0..7,
+ *   w_i = u32(t_{2i}) | u32(t_{2i+1}) << 32 over the block's tokens,
+ * with fmix64 the MurmurHash3 finaliser and a key of 0 replaced by 1.
+ * All prompts are matched against the table as it stood before the call
+ * (frozen snapshot): P_r = 16 * (length of the longest run of leading keys
+ * present), capped at floor((L_r - 1) / 16) blocks so that at least one token
+ * is recomputed.  Cached blocks reuse their registered ids; every other block
+ * of the prompt (and of its reserve) gets the next id of a bump allocator,
+ * prompt by prompt.  Afterwards the new full blocks are registered in prompt
+ * order, first registration winning.  ILPC_ENOSPC if ids would exceed
+ * num_blocks; ILPC_ETABLE if held keys + new full blocks would exceed the key
+ * capacity.  Synchronous, host only.
+ */
+int ilpc_prefix_match(ilpc_cache* cache, const int32_t* tokens, const int32_t* cu_seqlens,
+                      int32_t B, const int32_t* reserve, int32_t max_blocks, uint32_t flags,
+                      int32_t* cached_len, int32_t* block_tables, uint64_t* block_keys);
+
+/*
+ * Store the K/V of cache-missing tokens into the paged pools (section 3.2.2).
+ *
+ * k_new, v_new [device] bf16 [cu_new[B], Hkv, D]
+ * k_pool       [device] bf16 [num_blocks, Hkv, 16, D]
+ * v_pool       [device] bf16 [num_blocks, Hkv, D, 16]
+ * block_tables [device] int32 [B, max_blocks]
+ * cu_new       [device] int32 [B+1]   rows of request r: cu_new[r]..cu_new[r+1]
+ * start_pos    [device] int32 [B]     absolute position of request r's first row
+ * max_new      [host]   upper bound of cu_new[r+1]-cu_new[r] over r
+ *
+ * Row t of request r is written to position p = start_pos[r] + t, i.e. to
+ * logical block p/16, slot p%16.  Rows beyond max_new, and rows whose logical
+ * block is >= max_blocks or maps to an id outside [0, num_blocks), are not
+ * written (no out-of-bounds access is made).
+ */
+int ilpc_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                   uint16_t* v_pool, int32_t num_blocks, const int32_t* block_tables,
+                   int32_t max_blocks, const int32_t* cu_new, const int32_t* start_pos, int32_t B,
+                   int32_t max_new, int32_t Hkv, int32_t D, int32_t block_size, void* stream);
+
+/* Bytes of device workspace ilpc_paged_prefill_attn needs for these sizes
+ * (currently always 0: the kernels keep all state on chip). */
+int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                              size_t* bytes);
+
+/*
+ * Causal grouped-query attention of each request's newest q_len_r tokens
+ * over its whole context, read from the paged pools through the block table
+ * (section 2.1.2 prefill with reused prefix KV; a decode step is q_len_r = 1).
+ *
+ * q            [device] bf16 [cu_q[B], Hq, D]
+ * k_pool, v_pool as for ilpc_kv_append, already holding every context token
+ * block_tables [device] int32 [B, max_blocks]
+ * cu_q         [device] int32 [B+1]  query rows of request r: cu_q[r]..cu_q[r+1]
+ * seq_lens     [device] int32 [B]    context length L_r (cached + new tokens)
+ * max_q_len    [host]   >= every q_len_r; rows beyond it are not computed
+ * softmax_scale         multiplies q.k before the softmax (1/sqrt(D) usually)
+ * out          [device] bf16 [cu_q[B], Hq, D]
+ * workspace    [device] ilpc_attn_workspace_bytes() bytes, may be NULL if 0
+ *
+ * Query t of request r sits at position L_r - q_len_r + t and attends to keys
+ * 0 .. L_r - q_len_r + t; q head h reads kv head h / (Hq/Hkv).  Products and
+ * sums in fp32 (matrix cores take bf16 operands), online softmax in fp32,
+ * output rounded to bf16 (nearest-even).  A request with q_len_r > L_r, with
+ * L_r > 16 * max_blocks, or whose blocks map outside [0, num_blocks) gets
+ * unspecified output rows but causes no out-of-bounds access.
+ */
+int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                            int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                            const int32_t* cu_q, const int32_t* seq_lens, int32_t B,
+                            int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                            int32_t block_size, float softmax_scale, uint16_t* out,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ILPC_H */

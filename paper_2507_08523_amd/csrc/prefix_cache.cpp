@@ -1,0 +1,288 @@
+// Host side of the prefix cache: chained 64-bit keys of 16-token blocks, an
+// open-addressing key -> block-id table, and a bump block allocator.
+//
+// Block reuse follows InferLog section 2.1.2 ("KV Cache and Prefix Caching"):
+// a block's KV is reusable only when the block and every block before it carry
+// the same tokens, which a key chained over all preceding blocks captures.
+// A batch is matched against the table as it stood before the batch (frozen
+// snapshot), then its new full blocks are registered, first writer winning.
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/ilpc.h"
+#include "ilpc_internal.h"
+
+namespace ilpc {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+int set_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+namespace {
+
+constexpr int kBlock = 16;
+constexpr uint64_t kWordKey = 0x9E3779B97F4A7C15ull;  // golden-ratio word
+constexpr uint64_t kChainSeed = 0x243F6A8885A308D3ull;  // fractional digits of pi
+
+// MurmurHash3 64-bit finaliser (Appleby, public domain).
+inline uint64_t fmix64(uint64_t x) {
+  x ^= x >> 33;
+  x *= 0xFF51AFD7ED558CCDull;
+  x ^= x >> 33;
+  x *= 0xC4CEB9FE1A85EC53ull;
+  x ^= x >> 33;
+  return x;
+}
+
+// Digest of one block: eight 64-bit words, each position-keyed and mixed
+// independently (so the eight mixes overlap), summed, mixed once more.
+inline uint64_t block_digest(const int32_t* t) {
+  uint64_t acc = 0;
+  for (int i = 0; i < kBlock / 2; ++i) {
+    const uint64_t w = uint64_t(uint32_t(t[2 * i])) | (uint64_t(uint32_t(t[2 * i + 1])) << 32);
+    acc += fmix64(w ^ (uint64_t(i + 1) * kWordKey));
+  }
+  return fmix64(acc);
+}
+
+}  // namespace
+}  // namespace ilpc
+
+struct ilpc_cache {
+  int32_t num_blocks = 0;
+  int32_t next_block = 0;
+  uint64_t mask = 0;          // slots - 1
+  int64_t max_entries = 0;    // 7/8 of the slots
+  int64_t count = 0;
+  std::vector<uint64_t> keys;  // 0 marks an empty slot
+  std::vector<int32_t> vals;
+  std::vector<uint64_t> journal;  // slot of every registration, oldest first
+
+  // Slot holding `key`, or the empty slot where it would go.
+  uint64_t probe(uint64_t key) const {
+    uint64_t s = key & mask;
+    while (keys[s] != 0 && keys[s] != key) s = (s + 1) & mask;
+    return s;
+  }
+};
+
+using ilpc::set_error;
+
+extern "C" const char* ilpc_last_error(void) { return ilpc::g_last_error.c_str(); }
+
+extern "C" int ilpc_cache_create(int32_t num_blocks, int32_t block_size, int32_t table_log2_cap,
+                                 ilpc_cache** out) {
+  if (!out) return set_error(ILPC_EINVAL, "ilpc_cache_create: out is NULL");
+  *out = nullptr;
+  if (block_size != ilpc::kBlock)
+    return set_error(ILPC_EUNSUP, "ilpc_cache_create: block_size %d unsupported (16)", block_size);
+  if (num_blocks < 0) return set_error(ILPC_EINVAL, "ilpc_cache_create: num_blocks < 0");
+  if (table_log2_cap < 1 || table_log2_cap > 30)
+    return set_error(ILPC_EINVAL, "ilpc_cache_create: table_log2_cap %d not in [1, 30]",
+                     table_log2_cap);
+  ilpc_cache* c = new (std::nothrow) ilpc_cache();
+  if (!c) return set_error(ILPC_ENOSPC, "ilpc_cache_create: out of host memory");
+  const uint64_t slots = uint64_t(1) << table_log2_cap;
+  try {
+    c->keys.assign(slots, 0);
+    c->vals.assign(slots, -1);
+  } catch (...) {
+    delete c;
+    return set_error(ILPC_ENOSPC, "ilpc_cache_create: out of host memory");
+  }
+  c->num_blocks = num_blocks;
+  c->mask = slots - 1;
+  c->max_entries = int64_t(slots - slots / 8);
+  *out = c;
+  return ILPC_OK;
+}
+
+extern "C" void ilpc_cache_destroy(ilpc_cache* cache) { delete cache; }
+
+extern "C" int ilpc_cache_reset(ilpc_cache* cache) {
+  if (!cache) return set_error(ILPC_EINVAL, "ilpc_cache_reset: cache is NULL");
+  std::fill(cache->keys.begin(), cache->keys.end(), 0);
+  std::fill(cache->vals.begin(), cache->vals.end(), -1);
+  cache->count = 0;
+  cache->next_block = 0;
+  cache->journal.clear();
+  return ILPC_OK;
+}
+
+extern "C" int ilpc_cache_stats(const ilpc_cache* cache, int64_t stats[4]) {
+  if (!cache || !stats) return set_error(ILPC_EINVAL, "ilpc_cache_stats: NULL argument");
+  stats[0] = cache->count;
+  stats[1] = cache->next_block;
+  stats[2] = cache->max_entries;
+  stats[3] = cache->num_blocks;
+  return ILPC_OK;
+}
+
+extern "C" int ilpc_cache_checkpoint(const ilpc_cache* cache, int64_t mark[2]) {
+  if (!cache || !mark) return set_error(ILPC_EINVAL, "ilpc_cache_checkpoint: NULL argument");
+  mark[0] = int64_t(cache->journal.size());
+  mark[1] = cache->next_block;
+  return ILPC_OK;
+}
+
+extern "C" int ilpc_cache_rollback(ilpc_cache* cache, const int64_t mark[2]) {
+  if (!cache || !mark) return set_error(ILPC_EINVAL, "ilpc_cache_rollback: NULL argument");
+  if (mark[0] < 0 || mark[0] > int64_t(cache->journal.size()) || mark[1] < 0 ||
+      mark[1] > cache->next_block)
+    return set_error(ILPC_EINVAL, "ilpc_cache_rollback: mark is not from this cache's history");
+  // Removing the newest registrations first keeps every remaining key's probe
+  // run intact: each survivor was inserted before them, past older keys only.
+  while (int64_t(cache->journal.size()) > mark[0]) {
+    const uint64_t s = cache->journal.back();
+    cache->journal.pop_back();
+    cache->keys[s] = 0;
+    cache->vals[s] = -1;
+    --cache->count;
+  }
+  cache->next_block = int32_t(mark[1]);
+  return ILPC_OK;
+}
+
+extern "C" int ilpc_prefix_match(ilpc_cache* cache, const int32_t* tokens,
+                                 const int32_t* cu_seqlens, int32_t B, const int32_t* reserve,
+                                 int32_t max_blocks, uint32_t flags, int32_t* cached_len,
+                                 int32_t* block_tables, uint64_t* block_keys) {
+  using namespace ilpc;
+  if (!cache) return set_error(ILPC_EINVAL, "ilpc_prefix_match: cache is NULL");
+  if (B < 0) return set_error(ILPC_EINVAL, "ilpc_prefix_match: B < 0");
+  if (B == 0) return ILPC_OK;
+  if (!cu_seqlens || !cached_len || !block_tables)
+    return set_error(ILPC_EINVAL, "ilpc_prefix_match: NULL argument");
+  if (flags & ~(ILPC_NO_LOOKUP | ILPC_NO_REGISTER))
+    return set_error(ILPC_EINVAL, "ilpc_prefix_match: unknown flags 0x%x", flags);
+  if (max_blocks < 1) return set_error(ILPC_EINVAL, "ilpc_prefix_match: max_blocks < 1");
+  if (cu_seqlens[0] != 0) return set_error(ILPC_EINVAL, "ilpc_prefix_match: cu_seqlens[0] != 0");
+  if (!tokens) return set_error(ILPC_EINVAL, "ilpc_prefix_match: tokens is NULL");
+  const bool lookup = !(flags & ILPC_NO_LOOKUP);
+  const bool reg = !(flags & ILPC_NO_REGISTER);
+
+  // Validate every request before touching anything.
+  int64_t total_keys = 0;
+  for (int32_t r = 0; r < B; ++r) {
+    const int64_t L = int64_t(cu_seqlens[r + 1]) - cu_seqlens[r];
+    if (L < 1) return set_error(ILPC_EINVAL, "ilpc_prefix_match: request %d has length %lld", r,
+                                (long long)L);
+    const int64_t res = reserve ? reserve[r] : 0;
+    if (res < 0) return set_error(ILPC_EINVAL, "ilpc_prefix_match: request %d reserve < 0", r);
+    const int64_t n_total = (L + res + kBlock - 1) / kBlock;
+    if (n_total > max_blocks)
+      return set_error(ILPC_EINVAL, "ilpc_prefix_match: request %d needs %lld blocks > max_blocks %d",
+                       r, (long long)n_total, max_blocks);
+    total_keys += L / kBlock;
+  }
+
+  // Keys of every full block, and the matched run of each request (read-only pass).
+  std::vector<uint64_t> keys;
+  std::vector<int64_t> key_off(static_cast<size_t>(B) + 1);
+  std::vector<int32_t> matched(static_cast<size_t>(B));
+  std::vector<int32_t> hit_ids;
+  try {
+    keys.resize(size_t(total_keys));
+    hit_ids.reserve(size_t(total_keys));
+  } catch (...) {
+    return set_error(ILPC_ENOSPC, "ilpc_prefix_match: out of host memory");
+  }
+  std::vector<int64_t> hit_off(static_cast<size_t>(B) + 1);
+  int64_t ko = 0;
+  for (int32_t r = 0; r < B; ++r) {
+    const int32_t* t = tokens + cu_seqlens[r];
+    const int64_t L = int64_t(cu_seqlens[r + 1]) - cu_seqlens[r];
+    const int64_t n_full = L / kBlock, cap = (L - 1) / kBlock;
+    key_off[r] = ko;
+    uint64_t c = kChainSeed;
+    for (int64_t b = 0; b < n_full; ++b) {
+      c = fmix64(c ^ block_digest(t + b * kBlock));
+      if (c == 0) c = 1;
+      keys[size_t(ko + b)] = c;
+    }
+    hit_off[r] = int64_t(hit_ids.size());
+    int32_t m = 0;
+    if (lookup) {
+      while (m < cap) {
+        const uint64_t s = cache->probe(keys[size_t(ko + m)]);
+        if (cache->keys[s] == 0) break;
+        hit_ids.push_back(cache->vals[s]);
+        ++m;
+      }
+    }
+    matched[r] = m;
+    ko += n_full;
+  }
+  key_off[B] = ko;
+  hit_off[B] = int64_t(hit_ids.size());
+
+  // Capacity checks (pool, then key table) before any state change.
+  int64_t next = cache->next_block;
+  int64_t new_keys = 0;
+  for (int32_t r = 0; r < B; ++r) {
+    const int64_t L = int64_t(cu_seqlens[r + 1]) - cu_seqlens[r];
+    const int64_t res = reserve ? reserve[r] : 0;
+    next += (L + res + kBlock - 1) / kBlock - matched[r];
+    new_keys += L / kBlock - matched[r];
+  }
+  if (next > cache->num_blocks)
+    return set_error(ILPC_ENOSPC, "ilpc_prefix_match: batch needs %lld blocks, pool has %d",
+                     (long long)next, cache->num_blocks);
+  if (reg && cache->count + new_keys > cache->max_entries)
+    return set_error(ILPC_ETABLE, "ilpc_prefix_match: %lld held + %lld new keys > capacity %lld",
+                     (long long)cache->count, (long long)new_keys, (long long)cache->max_entries);
+
+  // Outputs: cached length, block table (hits, then fresh ids), keys.
+  int32_t alloc = cache->next_block;
+  for (int32_t r = 0; r < B; ++r) {
+    const int64_t L = int64_t(cu_seqlens[r + 1]) - cu_seqlens[r];
+    const int64_t res = reserve ? reserve[r] : 0;
+    const int32_t n_total = int32_t((L + res + kBlock - 1) / kBlock);
+    const int32_t n_full = int32_t(L / kBlock);
+    const int32_t m = matched[r];
+    int32_t* row = block_tables + int64_t(r) * max_blocks;
+    for (int32_t b = 0; b < m; ++b) row[b] = hit_ids[size_t(hit_off[r] + b)];
+    for (int32_t b = m; b < n_total; ++b) row[b] = alloc++;
+    for (int32_t b = n_total; b < max_blocks; ++b) row[b] = -1;
+    cached_len[r] = kBlock * m;
+    if (block_keys) {
+      uint64_t* krow = block_keys + int64_t(r) * max_blocks;
+      for (int32_t b = 0; b < n_full; ++b) krow[b] = keys[size_t(key_off[r] + b)];
+      for (int32_t b = n_full; b < max_blocks; ++b) krow[b] = 0;
+    }
+  }
+
+  // Commit: register new full blocks in request order, first writer wins.
+  if (reg) {
+    for (int32_t r = 0; r < B; ++r) {
+      const int32_t n_full = int32_t(key_off[r + 1] - key_off[r]);
+      const int32_t* row = block_tables + int64_t(r) * max_blocks;
+      for (int32_t b = matched[r]; b < n_full; ++b) {
+        const uint64_t key = keys[size_t(key_off[r] + b)];
+        const uint64_t s = cache->probe(key);
+        if (cache->keys[s] != 0) continue;
+        cache->keys[s] = key;
+        cache->vals[s] = row[b];
+        cache->journal.push_back(s);
+        ++cache->count;
+      }
+    }
+  }
+  cache->next_block = alloc;
+  return ILPC_OK;
+}

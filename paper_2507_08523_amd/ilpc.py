@@ -1,0 +1,216 @@
+"""ctypes binding of libilpc.so (C ABI in include/ilpc.h).
+
+Argument marshalling only: every step of the path runs in the library (host
+C++ prefix matching, HIP kernels for K/V append and attention).  Loading fails
+loudly if the library has not been built; there is no fallback.
+
+Device tensors are torch tensors (PyTorch supplies device memory and streams);
+they are checked for dtype, device, contiguity and shape before their
+pointers are handed over.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libilpc.so")
+
+OK, EINVAL, ENOSPC, ETABLE, EUNSUP, EHIP = 0, -1, -2, -3, -4, -5
+NO_LOOKUP, NO_REGISTER = 1, 2
+BLOCK = 16
+_NAMES = {EINVAL: "EINVAL", ENOSPC: "ENOSPC", ETABLE: "ETABLE", EUNSUP: "EUNSUP", EHIP: "EHIP"}
+
+# (name, restype, argtypes) of every exported symbol
+_i32, _u32, _i64, _f32, _vp = ctypes.c_int32, ctypes.c_uint32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+_SIGS = [
+    ("ilpc_last_error", ctypes.c_char_p, []),
+    ("ilpc_cache_create", _i32, [_i32, _i32, _i32, ctypes.POINTER(_vp)]),
+    ("ilpc_cache_destroy", None, [_vp]),
+    ("ilpc_cache_reset", _i32, [_vp]),
+    ("ilpc_cache_stats", _i32, [_vp, _vp]),
+    ("ilpc_cache_checkpoint", _i32, [_vp, _vp]),
+    ("ilpc_cache_rollback", _i32, [_vp, _vp]),
+    ("ilpc_prefix_match", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _u32, _vp, _vp, _vp]),
+    ("ilpc_kv_append", _i32, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
+                              _i32, _i32, _vp]),
+    ("ilpc_attn_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
+    ("ilpc_paged_prefill_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
+                                       _i32, _i32, _i32, _f32, _vp, _vp, ctypes.c_size_t, _vp]),
+]
+SYMBOLS = [s[0] for s in _SIGS]
+
+_lib = None
+
+
+class ILPCError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def load():
+    """The loaded library; raises if libilpc.so is missing (build it first)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ILPCError(EINVAL, f"{LIB_PATH} is missing: run `python -m paper_2507_08523_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, res, args in _SIGS:
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise ILPCError(rc, load().ilpc_last_error().decode())
+
+
+def _np_ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+class PrefixCache:
+    """Host prefix cache over a pool of ``num_blocks`` 16-token blocks."""
+
+    def __init__(self, num_blocks: int, table_log2_cap: int = 20):
+        lib = load()
+        h = ctypes.c_void_p()
+        _check(lib.ilpc_cache_create(num_blocks, BLOCK, table_log2_cap, ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().ilpc_cache_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    def reset(self):
+        _check(load().ilpc_cache_reset(self._h))
+
+    def stats(self) -> dict:
+        s = np.zeros(4, np.int64)
+        _check(load().ilpc_cache_stats(self._h, _np_ptr(s)))
+        return {"keys": int(s[0]), "next_block": int(s[1]), "capacity": int(s[2]), "num_blocks": int(s[3])}
+
+    def checkpoint(self) -> np.ndarray:
+        m = np.zeros(2, np.int64)
+        _check(load().ilpc_cache_checkpoint(self._h, _np_ptr(m)))
+        return m
+
+    def rollback(self, mark: np.ndarray):
+        m = np.ascontiguousarray(mark, dtype=np.int64)
+        _check(load().ilpc_cache_rollback(self._h, _np_ptr(m)))
+
+    def match(self, prompts, reserve=None, max_blocks=None, flags=0, want_keys=False, packed=None):
+        """Prefix-match a batch (list of int32 token arrays, or ``packed`` = (tokens, cu)).
+
+        Returns (cached_len int32[B], block_tables int32[B, max_blocks], keys or None).
+        """
+        if packed is not None:
+            tokens, cu = packed
+        else:
+            cu = np.zeros(len(prompts) + 1, np.int32)
+            cu[1:] = np.cumsum([len(p) for p in prompts])
+            tokens = np.concatenate(prompts).astype(np.int32) if prompts else np.zeros(0, np.int32)
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        cu = np.ascontiguousarray(cu, dtype=np.int32)
+        B = len(cu) - 1
+        res = None if reserve is None else np.ascontiguousarray(reserve, dtype=np.int32)
+        if max_blocks is None:
+            L = np.diff(cu).astype(np.int64) + (0 if res is None else res)
+            max_blocks = int(max(1, (L.max() + BLOCK - 1) // BLOCK)) if B else 1
+        cached = np.zeros(B, np.int32)
+        tables = np.zeros((B, max_blocks), np.int32)
+        keys = np.zeros((B, max_blocks), np.uint64) if want_keys else None
+        tok = tokens if tokens.size else np.zeros(1, np.int32)
+        _check(load().ilpc_prefix_match(self._h, _np_ptr(tok), _np_ptr(cu), B, _np_ptr(res), max_blocks,
+                                        flags, _np_ptr(cached), _np_ptr(tables), _np_ptr(keys)))
+        return cached, tables, keys
+
+
+# -- device steps ------------------------------------------------------------
+
+def _dev(t, dtype, name, ndim=None):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ILPCError(EINVAL, f"{name} must be a CUDA/HIP torch tensor")
+    if t.dtype != dtype:
+        raise ILPCError(EINVAL, f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ILPCError(EINVAL, f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ILPCError(EINVAL, f"{name} must have {ndim} dims, got {t.dim()}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def alloc_pools(num_blocks: int, n_kv_heads: int, head_dim: int, device="cuda"):
+    """Empty K pool [NB, Hkv, 16, D] and V pool [NB, Hkv, D, 16] (bf16)."""
+    import torch
+
+    k = torch.empty((num_blocks, n_kv_heads, BLOCK, head_dim), dtype=torch.bfloat16, device=device)
+    v = torch.empty((num_blocks, n_kv_heads, head_dim, BLOCK), dtype=torch.bfloat16, device=device)
+    return k, v
+
+
+def kv_append(k_new, v_new, k_pool, v_pool, block_tables, cu_new, start_pos, max_new: int, stream=None):
+    """Write packed new K/V rows [total, Hkv, D] into the pools (async on the stream)."""
+    import torch
+
+    NB, Hkv, bs, D = k_pool.shape
+    if v_pool.shape != (NB, Hkv, D, bs) or k_new.shape[1:] != (Hkv, D) or v_new.shape != k_new.shape:
+        raise ILPCError(EINVAL, "kv_append: inconsistent K/V/pool shapes")
+    B = cu_new.shape[0] - 1
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or start_pos.shape[0] != B:
+        raise ILPCError(EINVAL, "kv_append: inconsistent batch shapes")
+    args = (_dev(k_new, torch.bfloat16, "k_new", 3), _dev(v_new, torch.bfloat16, "v_new", 3),
+            _dev(k_pool, torch.bfloat16, "k_pool", 4), _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
+            _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],
+            _dev(cu_new, torch.int32, "cu_new", 1), _dev(start_pos, torch.int32, "start_pos", 1),
+            B, int(max_new), Hkv, D, bs, _stream(stream))
+    _check(load().ilpc_kv_append(*args))
+
+
+def attn_workspace_bytes(B, max_q_len, Hq, Hkv, D) -> int:
+    n = ctypes.c_size_t()
+    _check(load().ilpc_attn_workspace_bytes(B, max_q_len, Hq, Hkv, D, ctypes.byref(n)))
+    return int(n.value)
+
+
+def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_len: int, scale: float,
+                       out, workspace=None, stream=None):
+    """Causal GQA attention of packed queries [total, Hq, D] over the paged pools."""
+    import torch
+
+    NB, Hkv, bs, D = k_pool.shape
+    total, Hq, Dq = q.shape
+    B = cu_q.shape[0] - 1
+    if Dq != D or v_pool.shape != (NB, Hkv, D, bs) or out.shape != q.shape:
+        raise ILPCError(EINVAL, "paged_prefill_attn: inconsistent Q/K/V/out shapes")
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ILPCError(EINVAL, "paged_prefill_attn: inconsistent batch shapes")
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace", 1), workspace.numel()
+    args = (_dev(q, torch.bfloat16, "q", 3), _dev(k_pool, torch.bfloat16, "k_pool", 4),
+            _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
+            _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],
+            _dev(cu_q, torch.int32, "cu_q", 1), _dev(seq_lens, torch.int32, "seq_lens", 1), B,
+            int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3),
+            ws_ptr, ws_bytes, _stream(stream))
+    _check(load().ilpc_paged_prefill_attn(*args))

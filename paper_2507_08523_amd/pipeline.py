@@ -1,0 +1,122 @@
+"""One attention layer's prefix-cached prefill, step by step.
+
+    match   host C++ prefix matching (cached length + block table per prompt)
+    upload  one pinned host->device copy of the batch metadata
+    append  HIP kv_append of the cache-missing tokens' K/V
+    attend  HIP paged attention of the suffix queries
+
+The host state (prefix cache) and device state (K/V pools) live together in
+``PagedPrefixCache``.  PyTorch provides the device memory and the stream; all
+computation runs in libilpc.so.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import ilpc
+
+BLOCK = ilpc.BLOCK
+
+
+@dataclass
+class DeviceBatch:
+    """Device-side metadata of one batch (views into one int32 buffer)."""
+
+    block_tables: object   # int32 [B, max_blocks]
+    cu_q: object           # int32 [B+1]
+    seq_lens: object       # int32 [B]
+    start_pos: object      # int32 [B]
+    max_q_len: int
+    total_q: int
+    B: int
+
+
+class PagedPrefixCache:
+    """Prefix cache (host) + paged K/V pools (device) for one attention layer."""
+
+    def __init__(self, n_kv_heads: int, head_dim: int, num_blocks: int, max_blocks: int,
+                 max_batch: int, table_log2_cap: int = 20, device="cuda"):
+        import torch
+
+        self.n_kv_heads, self.head_dim = n_kv_heads, head_dim
+        self.num_blocks, self.max_blocks, self.max_batch = num_blocks, max_blocks, max_batch
+        self.device = torch.device(device)
+        self.cache = ilpc.PrefixCache(num_blocks, table_log2_cap)
+        self.k_pool, self.v_pool = ilpc.alloc_pools(num_blocks, n_kv_heads, head_dim, self.device)
+        n = max_batch * max_blocks + 3 * max_batch + 1
+        self._host = [torch.empty(n, dtype=torch.int32, pin_memory=True) for _ in range(2)]
+        self._host_ev = [None, None]
+        self._flip = 0
+        self._dev = torch.empty(n, dtype=torch.int32, device=self.device)
+
+    # -- host ---------------------------------------------------------------
+    def match(self, prompts=None, reserve=None, flags=0, packed=None):
+        return self.cache.match(prompts, reserve=reserve, max_blocks=self.max_blocks, flags=flags,
+                                packed=packed)[:2]
+
+    # -- host -> device -----------------------------------------------------
+    def upload(self, tables: np.ndarray, cu_q: np.ndarray, seq_lens: np.ndarray,
+               start_pos: np.ndarray, stream=None) -> DeviceBatch:
+        """Stage metadata in pinned memory and copy it with one async H2D copy."""
+        import torch
+
+        B = int(tables.shape[0])
+        if B > self.max_batch or tables.shape[1] != self.max_blocks:
+            raise ilpc.ILPCError(ilpc.EINVAL, "upload: batch larger than the staging buffers")
+        stream = stream or torch.cuda.current_stream(self.device)
+        i = self._flip
+        self._flip ^= 1
+        if self._host_ev[i] is not None:
+            self._host_ev[i].synchronize()  # the copy that last read this buffer is done
+        h = self._host[i]
+        nbt = B * self.max_blocks
+        hn = h.numpy()
+        hn[:nbt] = tables.reshape(-1)
+        hn[nbt:nbt + B + 1] = cu_q
+        hn[nbt + B + 1:nbt + 2 * B + 1] = seq_lens
+        hn[nbt + 2 * B + 1:nbt + 3 * B + 1] = start_pos
+        n = nbt + 3 * B + 1
+        with torch.cuda.stream(stream):
+            self._dev[:n].copy_(h[:n], non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(stream)
+        self._host_ev[i] = ev
+        d = self._dev
+        q_lens = np.diff(np.asarray(cu_q, dtype=np.int64))
+        return DeviceBatch(block_tables=d[:nbt].view(B, self.max_blocks), cu_q=d[nbt:nbt + B + 1],
+                           seq_lens=d[nbt + B + 1:nbt + 2 * B + 1],
+                           start_pos=d[nbt + 2 * B + 1:nbt + 3 * B + 1],
+                           max_q_len=int(q_lens.max()) if B else 0, total_q=int(cu_q[-1]) if B else 0,
+                           B=B)
+
+    def upload_prefill(self, cached_len, tables, seq_lens, stream=None) -> DeviceBatch:
+        """Metadata of a prefill: queries are positions cached_len[r]..seq_lens[r]-1."""
+        seq_lens = np.asarray(seq_lens, dtype=np.int32)
+        cached_len = np.asarray(cached_len, dtype=np.int32)
+        cu = np.zeros(len(seq_lens) + 1, np.int32)
+        cu[1:] = np.cumsum(seq_lens - cached_len)
+        return self.upload(tables, cu, seq_lens, cached_len, stream)
+
+    # -- device ---------------------------------------------------------------
+    def append(self, batch: DeviceBatch, k_new, v_new, stream=None):
+        ilpc.kv_append(k_new, v_new, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
+                       batch.start_pos, batch.max_q_len, stream)
+
+    def attend(self, batch: DeviceBatch, q, out, scale: float, stream=None):
+        ilpc.paged_prefill_attn(q, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
+                                batch.seq_lens, batch.max_q_len, scale, out, None, stream)
+
+
+def pool_blocks_needed(wl) -> int:
+    """Blocks a workload's warm + measured batches can allocate (no reuse assumed)."""
+    dec = wl.spec.decode_steps
+    n = sum(-(-len(p) // BLOCK) for p in wl.warm)
+    n += sum(-(-(len(p) + dec) // BLOCK) for p in wl.prompts)
+    return n + 1
+
+
+def max_blocks_of(wl) -> int:
+    dec = wl.spec.decode_steps
+    return max(-(-(len(p) + dec) // BLOCK) for p in wl.prompts)

@@ -1,0 +1,280 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerance on bf16 attention outputs: max |err| <= 2e-2 and mean |err| <= 2e-3
+against the float64 oracle on the same bf16 inputs.  Prefix lengths and block
+tables are compared bit-exactly, K/V appends by exact read-back.
+
+Small workloads are checked in full; the large ones run at full size in the
+same launch configuration the benchmark times, and sampled requests (the
+extremes of cached length and query length plus seeded picks) are checked.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.attn_ref import decode_step_ref, prefill_attention_ref
+from oracle.prefix_ref import PrefixCacheRef
+from paper_2507_08523_amd import ilpc, workload
+from paper_2507_08523_amd.pipeline import PagedPrefixCache, max_blocks_of, pool_blocks_needed
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 2e-2, 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm GPU (run with -m 'not gpu' on the CPU)")
+    ilpc.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+class Run:
+    """Warm + measured pass of one workload through the library."""
+
+    def __init__(self, spec, flags=0, perm_seed=None, table_log2_cap=20):
+        self.wl = wl = workload.build(spec)
+        wl.materialize("cuda")
+        sp = wl.spec
+        nb = pool_blocks_needed(wl)
+        self.pc = PagedPrefixCache(sp.n_kv_heads, sp.head_dim, nb, max_blocks_of(wl),
+                                   max(len(wl.prompts), len(wl.warm), 1), table_log2_cap)
+        self.perm = None
+        if perm_seed is not None:  # physical ids permuted: output must not change
+            self.perm = np.random.default_rng(perm_seed).permutation(nb).astype(np.int32)
+        self.ref_cache = PrefixCacheRef(nb, (1 << table_log2_cap) - (1 << table_log2_cap) // 8)
+        if wl.warm:
+            c, t = self.pc.match(wl.warm)
+            c_ref, t_ref, _ = self.ref_cache.match(wl.warm, max_blocks=self.pc.max_blocks)
+            assert np.array_equal(c, c_ref) and np.array_equal(t, t_ref)
+            rows = wl.packed_warm(c)
+            b = self.pc.upload_prefill(c, self._phys(t), [len(p) for p in wl.warm])
+            self.pc.append(b, rows["k_new"], rows["v_new"])
+        dec = sp.decode_steps
+        reserve = [dec] * len(wl.prompts) if dec else None
+        c, t = self.pc.match(wl.prompts, reserve=reserve, flags=flags)
+        c_ref, t_ref, _ = self.ref_cache.match(wl.prompts, reserve=reserve, max_blocks=self.pc.max_blocks,
+                                               no_lookup=bool(flags & 1), no_register=bool(flags & 2))
+        assert np.array_equal(c, c_ref), "cached lengths differ from the oracle"
+        assert np.array_equal(t, t_ref), "block tables differ from the oracle"
+        self.cached, self.tables = c, t
+        self.rows = wl.packed_suffix(c)
+        self.batch = self.pc.upload_prefill(c, self._phys(t), wl.seq_lens)
+        self.pc.append(self.batch, self.rows["k_new"], self.rows["v_new"])
+        self.out = torch.empty_like(self.rows["q"])
+        self.attend()
+
+    def _phys(self, t):
+        if self.perm is None:
+            return t
+        return np.where(t >= 0, self.perm[np.maximum(t, 0)], -1).astype(np.int32)
+
+    def attend(self):
+        self.pc.attend(self.batch, self.rows["q"], self.out, self.wl.spec.scale)
+        torch.cuda.synchronize()
+        return self.out
+
+    def request_rows(self, r):
+        cu = self.rows["cu"]
+        return self.out[int(cu[r]):int(cu[r + 1])]
+
+    def check(self, requests, tag=""):
+        wl = self.wl
+        worst, tot, cnt = 0.0, 0.0, 0
+        for r in requests:
+            L, P = int(wl.seq_lens[r]), int(self.cached[r])
+            k, v = wl.dense_kv(r, L)
+            q = wl.q_rows(r, P, L)
+            ref = prefill_attention_ref(q.float().cpu().numpy(), k.float().cpu().numpy(),
+                                        v.float().cpu().numpy(), wl.spec.scale)
+            got = self.request_rows(r).float().cpu().numpy()
+            assert np.isfinite(got).all(), f"request {r}: non-finite output"
+            err = np.abs(got - ref)
+            worst = max(worst, float(err.max()))
+            tot += float(err.sum())
+            cnt += err.size
+        mean = tot / max(cnt, 1)
+        log(f"[parity] {wl.spec.name}{tag}: {len(requests)} requests max_abs={worst:.3e} mean_abs={mean:.3e}")
+        assert worst <= MAX_ABS and mean <= MEAN_ABS
+        return worst, mean
+
+
+def _sample(run, n_rand, seed=0):
+    c = run.cached
+    S = run.wl.seq_lens - c
+    picks = {int(np.argmin(c)), int(np.argmax(c)), int(np.argmin(S)), int(np.argmax(S))}
+    rng = np.random.default_rng(seed)
+    picks |= {int(x) for x in rng.choice(len(c), size=min(n_rand, len(c)), replace=False)}
+    return sorted(picks)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b"])
+def test_prefill_full_check(name):
+    run = Run(name)
+    run.check(range(len(run.wl.prompts)))
+
+
+def test_qwen7b_full_size_sampled():
+    run = Run("qwen7b")
+    assert (run.wl.seq_lens - run.cached).min() >= 20
+    run.check(_sample(run, 4))
+
+
+@pytest.mark.parametrize("name", ["sweep0", "sweep25", "sweep50", "sweep75", "sweep100"])
+def test_sweep_full_size_sampled(name):
+    run = Run(name)
+    expect = {"sweep0": 0, "sweep25": 256, "sweep50": 496, "sweep75": 736, "sweep100": 976}[name]
+    assert (run.cached == expect).all()
+    run.check(_sample(run, 3))
+
+
+def test_large_prefill_then_decode_sampled():
+    run = Run("large")
+    wl, pc = run.wl, run.pc
+    picks = _sample(run, 1)
+    run.check(picks[:3])
+    B = len(wl.prompts)
+    L = wl.seq_lens.astype(np.int32)
+    cu = np.arange(B + 1, dtype=np.int32)
+    worst = 0.0
+    for s in range(wl.spec.decode_steps):
+        d = wl.decode_inputs(s)
+        b = pc.upload(run.tables, cu, L + s + 1, L + s)
+        pc.append(b, d["k_new"], d["v_new"])
+        out = torch.empty_like(d["q"])
+        pc.attend(b, d["q"], out, wl.spec.scale)
+        if s in (0, 13, wl.spec.decode_steps - 1):
+            torch.cuda.synchronize()
+            for r in picks:
+                k, v = wl.dense_kv(r, int(L[r]) + s + 1)
+                ref = decode_step_ref(d["q"][r].float().cpu().numpy(), k.float().cpu().numpy(),
+                                      v.float().cpu().numpy(), wl.spec.scale)
+                err = np.abs(out[r].float().cpu().numpy() - ref)
+                worst = max(worst, float(err.max()))
+                assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (s, r)
+    log(f"[parity] large decode: 32 steps, sampled max_abs={worst:.3e}")
+
+
+def test_kv_append_read_back_bit_exact():
+    run = Run(workload.scaled_spec("llama8b", 24))
+    bt = torch.from_numpy(run.tables).cuda().long()
+    for r in range(len(run.wl.prompts)):
+        P, L = int(run.cached[r]), int(run.wl.seq_lens[r])
+        pos = torch.arange(P, L, device="cuda")
+        blk = bt[r, pos // 16]
+        slot = pos % 16
+        k_rows = run.pc.k_pool[blk, :, slot, :]                 # [S, Hkv, D]
+        v_rows = run.pc.v_pool[blk, :, :, slot]                 # [S, Hkv, D]
+        cu = run.rows["cu"]
+        assert torch.equal(k_rows, run.rows["k_new"][int(cu[r]):int(cu[r + 1])])
+        assert torch.equal(v_rows, run.rows["v_new"][int(cu[r]):int(cu[r + 1])])
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_kv_append_partial_blocks_leave_neighbours(D):
+    # runs starting mid-block, single tokens, and a run spanning three blocks
+    torch.manual_seed(0)
+    Hkv, NB, MB = 2, 12, 4
+    k_pool = torch.full((NB, Hkv, 16, D), 7.0, dtype=torch.bfloat16, device="cuda")
+    v_pool = torch.full((NB, Hkv, D, 16), 7.0, dtype=torch.bfloat16, device="cuda")
+    starts, lens = [5, 0, 15, 31], [1, 16, 18, 2]
+    tables = torch.tensor([[0, 1, 2, 3], [4, 5, -1, -1], [6, 7, 8, -1], [9, 10, 11, -1]],
+                          dtype=torch.int32, device="cuda")
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device="cuda")
+    k_new = torch.randn(sum(lens), Hkv, D, device="cuda").to(torch.bfloat16)
+    v_new = torch.randn(sum(lens), Hkv, D, device="cuda").to(torch.bfloat16)
+    ilpc.kv_append(k_new, v_new, k_pool, v_pool, tables,
+                   cu, torch.tensor(starts, dtype=torch.int32, device="cuda"), max(lens))
+    torch.cuda.synchronize()
+    expect_k = torch.full_like(k_pool, 7.0)
+    expect_v = torch.full_like(v_pool, 7.0)
+    tb = tables.cpu().numpy()
+    row = 0
+    for r, (s, n) in enumerate(zip(starts, lens)):
+        for p in range(s, s + n):
+            b = int(tb[r, p // 16])
+            expect_k[b, :, p % 16, :] = k_new[row]
+            expect_v[b, :, :, p % 16] = v_new[row]
+            row += 1
+    assert torch.equal(k_pool, expect_k) and torch.equal(v_pool, expect_v)
+
+
+def test_prefix_cached_rows_bit_identical_to_full_prefill():
+    spec = workload.scaled_spec("llama8b", 16)
+    cached = Run(spec)
+    full = Run(spec, flags=ilpc.NO_LOOKUP)
+    assert (full.cached == 0).all() and (cached.cached > 0).all()
+    for r in range(len(cached.wl.prompts)):
+        P = int(cached.cached[r])
+        a = cached.request_rows(r)
+        b = full.request_rows(r)[P:]
+        assert torch.equal(a, b), r
+
+
+def test_physical_block_permutation_and_rerun_bit_identical():
+    spec = workload.scaled_spec("qwen7b", 12)
+    a = Run(spec)
+    b = Run(spec, perm_seed=3)
+    assert torch.equal(a.out, b.out)
+    first = a.out.clone()
+    assert torch.equal(a.attend(), first)
+
+
+def test_fully_cached_prompt_and_ragged_group():
+    # L % 16 == 0 and already registered: S = 16 recomputed; G = 7 columns
+    spec = workload.WorkloadSpec(name="capcase", n_q_heads=28, n_kv_heads=4, head_dim=128, n_prompts=3,
+                                 instr_len=96, n_demos=0, demo_len=0, pool_size=0, query_len=(0, 0),
+                                 warm="own_prefix", own_prefix_len=96, seed=9)
+    run = Run(spec)
+    assert (run.cached == 80).all()
+    run.check(range(3))
+
+
+def test_empty_and_zero_length_requests():
+    run = Run("tiny")
+    wl = run.wl
+    # B == 0 is a no-op
+    e = torch.zeros(0, wl.spec.n_q_heads, wl.spec.head_dim, dtype=torch.bfloat16, device="cuda")
+    z32 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ilpc.paged_prefill_attn(e, run.pc.k_pool, run.pc.v_pool,
+                            torch.zeros(0, run.pc.max_blocks, dtype=torch.int32, device="cuda"), z32,
+                            torch.zeros(0, dtype=torch.int32, device="cuda"), 0, wl.spec.scale, e.clone())
+    # requests 1 and 3 have no queries: the others are unchanged, nothing else is written
+    cu = run.rows["cu"].copy()
+    keep = [0, 2]
+    rows = torch.cat([run.request_rows(r) for r in keep])
+    qs = torch.cat([run.rows["q"][int(cu[r]):int(cu[r + 1])] for r in keep])
+    new_cu = np.array([0, 32, 32, 64, 64], np.int32)
+    out = torch.full_like(qs, float("nan"))
+    ilpc.paged_prefill_attn(qs, run.pc.k_pool, run.pc.v_pool, run.batch.block_tables,
+                            torch.from_numpy(new_cu).cuda(), run.batch.seq_lens, 32, wl.spec.scale, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out, rows)
+
+
+def test_abi_rejects_bad_arguments_on_device():
+    # every case is refused by host-side validation before any launch
+    run = Run("tiny")
+    b, pc, q = run.batch, run.pc, run.rows["q"]
+    lib = ilpc.load()
+
+    def call(q_ptr, Hq, Hkv, D):
+        return lib.ilpc_paged_prefill_attn(q_ptr, pc.k_pool.data_ptr(), pc.v_pool.data_ptr(),
+                                           pc.num_blocks, b.block_tables.data_ptr(), pc.max_blocks,
+                                           b.cu_q.data_ptr(), b.seq_lens.data_ptr(), b.B, b.max_q_len,
+                                           Hq, Hkv, D, 16, 0.125, run.out.data_ptr(), None, 0, None)
+
+    assert call(q.data_ptr(), 4, 1, 96) == ilpc.EUNSUP       # head_dim
+    assert call(q.data_ptr() + 2, 4, 1, 64) == ilpc.EINVAL   # misaligned Q
+    assert call(q.data_ptr(), 6, 4, 64) == ilpc.EUNSUP       # Hq % Hkv != 0
+    assert call(None, 4, 1, 64) == ilpc.EINVAL               # NULL
+    assert lib.ilpc_last_error().decode()

@@ -1,0 +1,191 @@
+"""Host logic of libilpc.so on the CPU: exports, and prefix matching bit-exact
+against the oracle (cached lengths, block tables and block keys).
+
+No GPU is touched: the library is loaded and only host entry points are called.
+"""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle.prefix_ref import BLOCK, OracleError, PrefixCacheRef, chain_keys
+from paper_2507_08523_amd import ilpc, workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ilpc.LIB_PATH):
+        pytest.fail("libilpc.so is not built: run `python -m paper_2507_08523_amd.build`")
+    return ilpc.load()
+
+
+def test_library_exports_every_declared_symbol(lib):
+    with open(os.path.join(ROOT, "include", "ilpc.h")) as f:
+        decl = set(re.findall(r"\b(ilpc_\w+)\s*\(", f.read()))
+    assert decl == set(ilpc.SYMBOLS)
+    for name in decl:
+        assert hasattr(lib, name), name
+
+
+def _run_both(batches, num_blocks=1 << 16, log2cap=18, reserve_fn=None, max_blocks=None, flags=0):
+    ref = PrefixCacheRef(num_blocks=num_blocks, max_entries=(1 << log2cap) - (1 << log2cap) // 8)
+    cache = ilpc.PrefixCache(num_blocks, log2cap)
+    for i, prompts in enumerate(batches):
+        res = reserve_fn(i, prompts) if reserve_fn else None
+        mb = max_blocks or max(-(-(len(p) + (res[j] if res else 0)) // BLOCK) for j, p in enumerate(prompts))
+        c_ref, t_ref, k_ref = ref.match(prompts, reserve=res, max_blocks=mb,
+                                        no_lookup=bool(flags & 1), no_register=bool(flags & 2))
+        c, t, k = cache.match(prompts, reserve=res, max_blocks=mb, flags=flags, want_keys=True)
+        assert np.array_equal(c, c_ref), i
+        assert np.array_equal(t, t_ref), i
+        assert np.array_equal(k, k_ref), i
+        st = cache.stats()
+        assert st["keys"] == len(ref.table) and st["next_block"] == ref.next_block
+    return ref, cache
+
+
+def test_golden_key_vectors_match(lib):
+    path = os.path.join(ROOT, "tests", "golden", "chain_keys.txt")
+    cache = ilpc.PrefixCache(4096, 12)
+    with open(path) as f:
+        for line in f:
+            if line.startswith("#"):
+                continue
+            head, _, keys = line.rstrip("\n").split(" | ")
+            parts = head.split()
+            toks = np.array([int(x) for x in parts[2:2 + int(parts[1])]], dtype=np.int32)
+            _, _, k = cache.match([toks], want_keys=True, flags=ilpc.NO_REGISTER)
+            n_full = len(toks) // BLOCK
+            assert [f"{int(x):016x}" for x in k[0, :n_full]] == keys.split(), parts[0]
+
+
+@pytest.mark.parametrize("name", list(workload.SPECS))
+def test_workload_batches_bit_exact(lib, name):
+    wl = workload.build(name)
+    batches = ([wl.warm] if wl.warm else []) + [wl.prompts]
+    dec = wl.spec.decode_steps
+    _run_both(batches, num_blocks=1 << 20, log2cap=20,
+              reserve_fn=lambda i, p: [dec] * len(p) if dec else None)
+
+
+def test_random_batches_with_reuse_bit_exact(lib):
+    rng = np.random.default_rng(21)
+    pieces = [rng.integers(0, 32000, int(rng.integers(3, 50))).astype(np.int32) for _ in range(8)]
+    batches = []
+    for _ in range(12):
+        batch = []
+        for _ in range(int(rng.integers(1, 9))):
+            order = rng.permutation(len(pieces))[: int(rng.integers(1, 5))]
+            tail = rng.integers(-5, 32000, int(rng.integers(0, 30))).astype(np.int32)
+            p = np.concatenate([pieces[i] for i in order] + [tail])
+            batch.append(p if len(p) else np.array([1], np.int32))
+        if rng.random() < 0.3:
+            batch.append(batch[0].copy())
+        batches.append(batch)
+    ref, _ = _run_both(batches, reserve_fn=lambda i, p: [int(x) for x in rng.integers(0, 40, len(p))])
+    assert len(ref.table) > 0
+
+
+@pytest.mark.parametrize("flags", [ilpc.NO_LOOKUP, ilpc.NO_REGISTER, ilpc.NO_LOOKUP | ilpc.NO_REGISTER])
+def test_flags_bit_exact(lib, flags):
+    wl = workload.build(workload.scaled_spec("llama8b", 12))
+    ref = PrefixCacheRef(1 << 16, (1 << 14) - (1 << 11))
+    cache = ilpc.PrefixCache(1 << 16, 14)
+    ref.match(wl.warm)
+    cache.match(wl.warm)
+    c_ref, t_ref, _ = ref.match(wl.prompts, no_lookup=bool(flags & 1), no_register=bool(flags & 2))
+    c, t, _ = cache.match(wl.prompts, flags=flags)
+    assert np.array_equal(c, c_ref) and np.array_equal(t, t_ref)
+    assert cache.stats()["keys"] == len(ref.table)
+
+
+def test_fully_cached_prompt_cap(lib):
+    p = np.arange(64, dtype=np.int32)
+    cache = ilpc.PrefixCache(64, 8)
+    _, t0, _ = cache.match([p])
+    c, t, _ = cache.match([p])
+    assert c[0] == 48 and t[0, 3] != t0[0, 3] and list(t[0, :3]) == list(t0[0, :3])
+
+
+def test_empty_batch_is_a_noop(lib):
+    cache = ilpc.PrefixCache(16, 6)
+    c, t, _ = cache.match([])
+    assert c.shape == (0,) and cache.stats()["next_block"] == 0
+
+
+@pytest.mark.parametrize("what,code", [("pool", ilpc.ENOSPC), ("table", ilpc.ETABLE),
+                                       ("empty", ilpc.EINVAL), ("max_blocks", ilpc.EINVAL),
+                                       ("reserve", ilpc.EINVAL), ("flags", ilpc.EINVAL)])
+def test_errors_match_oracle_and_leave_state(lib, what, code):
+    # capacity 4 slots -> 3 keys; pool 8 blocks
+    cache = ilpc.PrefixCache(8, 2)
+    ref = PrefixCacheRef(8, 3)
+    first = [np.arange(20, dtype=np.int32)]
+    cache.match(first)
+    ref.match(first)
+    before = cache.stats()
+    p = np.arange(100, 180, dtype=np.int32)
+    kw = {}
+    if what == "pool":
+        batch = [p[:40], p[:70] + 1]
+    elif what == "table":
+        batch = [p[:70]]
+    elif what == "empty":
+        batch = [p[:20], np.zeros(0, np.int32)]
+    elif what == "max_blocks":
+        batch, kw = [p], {"max_blocks": 4}
+    elif what == "reserve":
+        batch, kw = [p[:20]], {"reserve": [-1]}
+    else:
+        batch, kw = [p[:20]], {"flags": 4}
+    with pytest.raises(ilpc.ILPCError) as e:
+        cache.match(batch, **kw)
+    assert e.value.code == code
+    assert cache.stats() == before
+    assert ilpc.load().ilpc_last_error().decode()
+    if what != "flags":
+        with pytest.raises(OracleError):
+            ref.match(batch, **{k: v for k, v in kw.items()})
+
+
+def test_checkpoint_rollback_restores_matching(lib):
+    wl = workload.build(workload.scaled_spec("llama8b", 16))
+    cache = ilpc.PrefixCache(1 << 14, 14)
+    cache.match(wl.warm)
+    mark = cache.checkpoint()
+    s0 = cache.stats()
+    c1, t1, _ = cache.match(wl.prompts)
+    assert cache.stats()["keys"] > s0["keys"]
+    cache.rollback(mark)
+    assert cache.stats() == s0
+    c2, t2, _ = cache.match(wl.prompts)
+    assert np.array_equal(c1, c2) and np.array_equal(t1, t2)
+    with pytest.raises(ilpc.ILPCError):
+        cache.rollback(np.array([10 ** 9, 0], np.int64))
+
+
+def test_rollback_keeps_older_probe_runs(lib):
+    # a tiny table forces long probe runs; undoing the newest keys must not
+    # hide older keys that probed past them
+    rng = np.random.default_rng(5)
+    cache = ilpc.PrefixCache(1 << 12, 7)   # 128 slots, 112 keys
+    old = [rng.integers(0, 32000, 16 * 3 + 1).astype(np.int32) for _ in range(20)]
+    cache.match(old)
+    mark = cache.checkpoint()
+    new = [rng.integers(0, 32000, 16 * 4 + 1).astype(np.int32) for _ in range(10)]
+    cache.match(new)
+    cache.rollback(mark)
+    c, _, _ = cache.match(old, flags=ilpc.NO_REGISTER)
+    assert (c == 48).all()
+    c, _, _ = cache.match(new, flags=ilpc.NO_REGISTER)
+    assert (c == 0).all()
+
+
+def test_keys_are_never_zero_and_chain(lib):
+    toks = np.arange(16 * 5 + 3, dtype=np.int32)
+    _, _, k = ilpc.PrefixCache(64, 8).match([toks], want_keys=True)
+    assert [int(x) for x in k[0, :5]] == chain_keys(toks)
+    assert (k[0, :5] != 0).all() and (k[0, 5:] == 0).all()
