@@ -1,0 +1,268 @@
+"""Benchmark of the prefix-cached prefill hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic
+log-parsing prompts (inputs already resident in HBM):
+
+    prefix match (host C++)  ->  one pinned H2D copy of the batch metadata
+    ->  kv_append (HIP)  ->  paged prefill attention (HIP)
+    [-> decode steps, for workloads that have them: kv_append of one token per
+        prompt + attention with one query per prompt, 32 times]
+
+Every step starts from the same cache state: the step takes a checkpoint
+before matching and rolls the cache back after its metadata is staged (the
+rollback is extra host work inside the step, nothing is skipped).
+
+Prints ONE JSON line.  ``value`` is new-query tokens per second over the timed
+steps (prefill suffix tokens + decode tokens).  ``roofline`` is for the
+dominant kernel, the prefill attention launch, timed with HIP events on the
+stream it runs on.  ``cpu_baseline`` times the fp64 oracle on a bounded
+sample of the same workload on the host cores.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prefix-cached prefill attn: query tokens/s, TFLOP/s & GB/s vs MI355X roofline"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak
+KERNEL_SRC = os.path.join(ROOT, "paper_2507_08523_amd", "csrc", "paged_attn.hip")
+
+
+def workload_work(wl, cached_len):
+    """Algorithmic FLOPs and bytes of one prefill attention launch."""
+    sp = wl.spec
+    L = wl.seq_lens.astype(np.float64)
+    P = np.asarray(cached_len, dtype=np.float64)
+    S = L - P
+    pairs = float(np.sum(S * P + S * (S + 1) / 2))   # visible (query, key) pairs
+    flops = 4.0 * sp.n_q_heads * sp.head_dim * pairs
+    kv_bytes = float(np.sum(4.0 * sp.n_kv_heads * sp.head_dim * L))   # K + V context, bf16
+    qo_bytes = float(np.sum(4.0 * sp.n_q_heads * sp.head_dim * S))     # Q in + O out, bf16
+    return {"pairs": pairs, "flops": flops, "logical_bytes": kv_bytes + qo_bytes,
+            "query_tokens": int(S.sum())}
+
+
+def kernel_source_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_profile(workload_name: str):
+    """Measured HBM bytes per launch from committed counter runs, if still current."""
+    path = os.path.join(ROOT, "profiles", f"paged_attn_{workload_name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha") != kernel_source_sha():
+        return None  # kernel changed since the counters were taken
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, cached_len, budget_s: float):
+    """Time the fp64 oracle (prefix match of the whole batch + attention of as
+    many requests as fit the budget) on the host cores."""
+    from threadpoolctl import threadpool_info
+
+    from oracle.attn_ref import prefill_attention_ref
+    from oracle.prefix_ref import PrefixCacheRef
+
+    ref = PrefixCacheRef(1 << 30, 1 << 30)
+    if wl.warm:
+        ref.match(wl.warm)
+    t0 = time.perf_counter()
+    c_ref, _, _ = ref.match(wl.prompts)
+    t_match = time.perf_counter() - t0
+    assert np.array_equal(c_ref, cached_len)
+    rng = np.random.default_rng(0)
+    order = rng.permutation(len(wl.prompts))
+    t_attn, tokens, done = 0.0, 0, 0
+    for r in order:
+        L, P = int(wl.seq_lens[r]), int(cached_len[r])
+        k, v = wl.dense_kv(int(r), L)
+        q = wl.q_rows(int(r), P, L).float().cpu().numpy().astype(np.float64)
+        k = k.float().cpu().numpy().astype(np.float64)
+        v = v.float().cpu().numpy().astype(np.float64)
+        t0 = time.perf_counter()
+        prefill_attention_ref(q, k, v, wl.spec.scale)
+        t_attn += time.perf_counter() - t0
+        tokens += L - P
+        done += 1
+        if t_attn >= budget_s:
+            break
+    total_q = int(np.sum(wl.seq_lens - cached_len))
+    sec_per_token = t_match / total_q + t_attn / tokens
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] + [1])
+    return {"value": 1.0 / sec_per_token, "unit": "query tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"fp64 oracle: prefix match of all {len(wl.prompts)} prompts ({t_match*1e3:.1f} ms) + "
+                       f"attention of {done} of {len(wl.prompts)} requests ({tokens} query tokens, "
+                       f"{t_attn:.1f} s); host nproc={os.cpu_count()}")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle attention to time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path needs no collective "
+              "and every box here has one GPU", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2507_08523_amd import ilpc, workload
+    from paper_2507_08523_amd.pipeline import PagedPrefixCache, max_blocks_of, pool_blocks_needed
+
+    ilpc.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    wl = workload.build(args.workload)
+    wl.materialize(dev)
+    sp = wl.spec
+    pc = PagedPrefixCache(sp.n_kv_heads, sp.head_dim, pool_blocks_needed(wl), max_blocks_of(wl),
+                          max(len(wl.prompts), len(wl.warm), 1), 20, dev)
+
+    # warm pass (untimed): registers the shared prefix blocks and their K/V
+    if wl.warm:
+        c, t = pc.match(wl.warm)
+        rows = wl.packed_warm(c)
+        pc.append(pc.upload_prefill(c, t, [len(p) for p in wl.warm]), rows["k_new"], rows["v_new"])
+        torch.cuda.synchronize()
+        del rows
+
+    tokens = np.concatenate(wl.prompts).astype(np.int32)
+    cu_tok = np.zeros(len(wl.prompts) + 1, np.int32)
+    cu_tok[1:] = np.cumsum(wl.seq_lens)
+    dec = sp.decode_steps
+    reserve = np.full(len(wl.prompts), dec, np.int32) if dec else None
+
+    # rehearsal: learn the cached lengths, gather the suffix inputs (resident in HBM)
+    mark = pc.cache.checkpoint()
+    cached, tables = pc.match(packed=(tokens, cu_tok), reserve=reserve)
+    pc.cache.rollback(mark)
+    rows = wl.packed_suffix(cached)
+    q, k_new, v_new = rows["q"], rows["k_new"], rows["v_new"]
+    out = torch.empty_like(q)
+    L = wl.seq_lens.astype(np.int32)
+    dec_in = [wl.decode_inputs(s) for s in range(dec)]
+    dec_out = [torch.empty_like(d["q"]) for d in dec_in]
+    cu_dec = np.arange(len(L) + 1, dtype=np.int32)
+    work = workload_work(wl, cached)
+    n_tokens = work["query_tokens"] + dec * len(L)
+
+    n_ev = args.steps + args.warmup
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
+    host_s = []
+
+    def step(i):
+        e = ev[i]
+        h0 = time.perf_counter()
+        m = pc.cache.checkpoint()
+        c, t = pc.match(packed=(tokens, cu_tok), reserve=reserve)
+        b = pc.upload_prefill(c, t, L, stream)
+        pc.cache.rollback(m)
+        host_s.append(time.perf_counter() - h0)
+        e[0].record(stream)
+        pc.append(b, k_new, v_new, stream)
+        e[1].record(stream)
+        pc.attend(b, q, out, sp.scale, stream)
+        e[2].record(stream)
+        for s in range(dec):
+            bd = pc.upload(t, cu_dec, L + s + 1, L + s, stream)
+            pc.append(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], stream)
+            pc.attend(bd, dec_in[s]["q"], dec_out[s], sp.scale, stream)
+        e[3].record(stream)
+        return c
+
+    for i in range(args.warmup):
+        c = step(i)
+    torch.cuda.synchronize()
+    assert np.array_equal(c, cached), "cached lengths changed between steps"
+    host_s.clear()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, n_ev):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    timed = ev[args.warmup:]
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in timed]))
+    append_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in timed]))
+    decode_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in timed])) if dec else 0.0
+    ms_per_step = elapsed * 1e3 / args.steps
+    tflops = work["flops"] / (attn_ms * 1e-3) / 1e12
+    gbs = work["logical_bytes"] / (attn_ms * 1e-3) / 1e9
+    # the prefill launch is bound by whichever roofline limit is higher for it
+    t_mfma = work["flops"] / (PEAK_BF16_TFLOPS * 1e12)
+    t_hbm = work["logical_bytes"] / (PEAK_HBM_GBS * 1e9)
+    traffic = traffic_from_profile(args.workload)
+    if t_mfma >= t_hbm:
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic}
+
+    line = {
+        "metric": METRIC,
+        "value": round(n_tokens * args.steps / elapsed, 1),
+        "unit": "query tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": sp.name, "prompts": len(wl.prompts), "q_heads": sp.n_q_heads,
+                   "kv_heads": sp.n_kv_heads, "head_dim": sp.head_dim, "block": 16,
+                   "query_tokens": work["query_tokens"], "decode_steps": dec,
+                   "cached_fraction": round(float(cached.sum() / wl.seq_lens.sum()), 4)},
+        "roofline": roof,
+        "attn": {"launch_us": round(attn_ms * 1e3, 2), "tflops": round(tflops, 2),
+                 "logical_gbs": round(gbs, 1), "flops": work["flops"], "logical_bytes": work["logical_bytes"],
+                 "kernel_sha": kernel_source_sha()},
+        "breakdown_ms": {"host_match_upload": round(float(np.mean(host_s)) * 1e3, 4),
+                         "kv_append": round(append_ms, 4), "attention": round(attn_ms, 4),
+                         "decode_steps": round(decode_ms, 4)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, cached, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -30,6 +30,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -107,13 +108,20 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// paged attention: grid (column tiles, kv heads, requests), heaviest tile first.
+// paged attention.  1-D grid over (column tile, kv head, request) work items,
+// heaviest column tile of a (request, kv head) first.  Work items are spread
+// so that those sharing one (request, kv head) -- and so the same K/V blocks --
+// land on the same XCD (workgroups are dealt round-robin to the 8 XCDs, each
+// with its own L2).
+constexpr int kIdWin = 256;        // block ids of the current window, cached in LDS
+constexpr float kLazyRescale = 8.f;  // log2 growth of a column max tolerated before rescaling O
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void paged_attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
     const uint16_t* __restrict__ v_pool, int num_blocks, const int32_t* __restrict__ block_tables,
     int max_blocks, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int Hq,
-    int Hkv, float scale_log2, uint16_t* __restrict__ out) {
+    int Hkv, int n_col_tiles, float scale_log2, uint16_t* __restrict__ out) {
   constexpr int kDch = D / 16;         // 16-wide contraction chunks of Q.K^T
   constexpr int kDt = D / 32;          // 32-row output tiles of O^T
   constexpr int kRowBytes = D * 2;     // one K row in LDS
@@ -122,15 +130,24 @@ __global__ __launch_bounds__(kThreads, 2) void paged_attn_kernel(
   constexpr int kVLoads = kTileBlocks * 2 * D / kThreads;
   constexpr int kVBlockBytes = D * 32;  // one [D][16] V block in LDS
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * kKeys * D * 2];
+  __shared__ int32_t s_ids[kIdWin];
   uint8_t* const sK = smem;
   uint8_t* const sV = smem + kKeys * D * 2;
 
-  const int r = blockIdx.z, kvh = blockIdx.y;
+  // XCD-aware decode of the work item.
+  const unsigned n_items = gridDim.x, bid = blockIdx.x;
+  const unsigned xcd = bid & 7u, per = n_items >> 3, extra = n_items & 7u;
+  const unsigned w = xcd * per + min(xcd, extra) + (bid >> 3);
+  const int tile = n_col_tiles - 1 - int(w % unsigned(n_col_tiles));
+  const unsigned rest = w / unsigned(n_col_tiles);
+  const int kvh = int(rest % unsigned(Hkv));
+  const int r = int(rest / unsigned(Hkv));
+
   const int G = Hq / Hkv;
   const int q0 = cu_q[r];
   const int q_len = cu_q[r + 1] - q0;
   const int n_cols = q_len * G;
-  const int col0 = int(gridDim.x - 1 - blockIdx.x) * kCols;
+  const int col0 = tile * kCols;
   int L = seq_lens[r];
   if (L > max_blocks * kBlock) L = max_blocks * kBlock;
   if (q_len <= 0 || col0 >= n_cols || q_len > L) return;
@@ -153,53 +170,52 @@ __global__ __launch_bounds__(kThreads, 2) void paged_attn_kernel(
   const int wave_pos_max = qstart + min(wave_first + kColsPerWave - 1, n_cols - 1) / G;
   const int wg_pos_max = qstart + min(col0 + kCols - 1, n_cols - 1) / G;
   const int n_tiles = wg_pos_max / kKeys + 1;
+  const int n_blk_used = (wg_pos_max >> 4) + 1;  // <= ceil(L / 16) <= max_blocks
 
   bf16x8 qf[kDch];
 #pragma unroll
   for (int kc = 0; kc < kDch; ++kc) qf[kc] = as_bf16x8(*(const u32x4*)(q + qrow + kc * 16 + hh * 8));
 
   const int32_t* bt = block_tables + size_t(r) * max_blocks;
-  u32x4 kreg[kKLoads], vreg[kVLoads];
+  // Block ids [base, base + kIdWin) -> LDS; ids outside the pool become -1.
+  auto fill_ids = [&](int base) {
+    for (int i = tid; i < kIdWin; i += kThreads) {
+      const int lb = base + i;
+      int id = -1;
+      if (lb < n_blk_used) {
+        id = bt[lb];
+        if (id < 0 || id >= num_blocks) id = -1;
+      }
+      s_ids[i] = id;
+    }
+  };
+  auto win_base = [](int j0) { return ((j0 >> 4) / kIdWin) * kIdWin; };
 
+  u32x4 kreg[kKLoads], vreg[kVLoads];
+  // Issue the global loads of one tile; nothing here waits on their data.
+  // Unusable block ids read block 0 instead: stray K rows only ever meet
+  // masked scores, stray V rows are zeroed when the tile is stored.
   auto load_tile = [&](int j0) {
+    const int wb = win_base(j0);
 #pragma unroll
     for (int it = 0; it < kKLoads; ++it) {
       const int idx = it * kThreads + tid;
       const int key = idx / kKch, c = idx % kKch;
-      const int j = j0 + key;
-      const int lb = j >> 4;
-      const int phys = lb < max_blocks ? bt[lb] : -1;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (j < L && phys >= 0 && phys < num_blocks)
-        v = *(const u32x4*)(k_pool + ((size_t(phys) * Hkv + kvh) * kBlock + (j & 15)) * D + c * 8);
-      kreg[it] = v;
+      const int id = max(s_ids[(j0 >> 4) + (key >> 4) - wb], 0);
+      kreg[it] = *(const u32x4*)(k_pool + ((size_t(id) * Hkv + kvh) * kBlock + (key & 15)) * D + c * 8);
     }
 #pragma unroll
     for (int it = 0; it < kVLoads; ++it) {
       const int idx = it * kThreads + tid;
       const int kb = idx / (2 * D), rem = idx % (2 * D);
       const int d = rem >> 1, hf = rem & 1;
-      const int jb = j0 + kb * kBlock + hf * 8;
-      const int lb = jb >> 4;
-      const int phys = lb < max_blocks ? bt[lb] : -1;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (jb < L && phys >= 0 && phys < num_blocks) {
-        v = *(const u32x4*)(v_pool + ((size_t(phys) * Hkv + kvh) * D + d) * kBlock + hf * 8);
-        const int nvalid = L - jb;  // keys past the context are zeroed: P = 0 must not meet NaN
-        if (nvalid < 8) {
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const uint32_t keep = (2 * w < nvalid ? 0x0000FFFFu : 0u) |
-                                  (2 * w + 1 < nvalid ? 0xFFFF0000u : 0u);
-            v[w] &= keep;
-          }
-        }
-      }
-      vreg[it] = v;
+      const int id = max(s_ids[(j0 >> 4) + kb - wb], 0);
+      vreg[it] = *(const u32x4*)(v_pool + ((size_t(id) * Hkv + kvh) * D + d) * kBlock + hf * 8);
     }
   };
 
-  auto store_tile = [&]() {
+  auto store_tile = [&](int j0) {
+    const int wb = win_base(j0);
 #pragma unroll
     for (int it = 0; it < kKLoads; ++it) {
       const int idx = it * kThreads + tid;
@@ -212,7 +228,16 @@ __global__ __launch_bounds__(kThreads, 2) void paged_attn_kernel(
       const int idx = it * kThreads + tid;
       const int kb = idx / (2 * D), rem = idx % (2 * D);
       const int d = rem >> 1, hf = rem & 1;
-      *(u32x4*)(sV + kb * kVBlockBytes + d * 32 + ((hf ^ ((d >> 2) & 1)) << 4)) = vreg[it];
+      const int jb = j0 + kb * kBlock + hf * 8;
+      // keys past the context (or in an unusable block) are zeroed: P = 0 must not meet NaN
+      const int nvalid = s_ids[(j0 >> 4) + kb - wb] < 0 ? 0 : L - jb;
+      u32x4 v = vreg[it];
+      if (nvalid < 8) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          v[e] &= (2 * e < nvalid ? 0x0000FFFFu : 0u) | (2 * e + 1 < nvalid ? 0xFFFF0000u : 0u);
+      }
+      *(u32x4*)(sV + kb * kVBlockBytes + d * 32 + ((hf ^ ((d >> 2) & 1)) << 4)) = v;
     }
   };
 
@@ -221,79 +246,98 @@ __global__ __launch_bounds__(kThreads, 2) void paged_attn_kernel(
   for (int dt = 0; dt < kDt; ++dt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) o[dt][i] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_used = -INFINITY;  // max (log2 units) the exponentials of this column are taken against
+  float l_run = 0.f;         // this lane half's share of the column's exponential sum
+  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
 
+  fill_ids(0);
+  __syncthreads();
   load_tile(0);
   for (int kt = 0; kt < n_tiles; ++kt) {
     const int j0 = kt * kKeys;
     __syncthreads();
-    store_tile();
+    store_tile(j0);
+    const bool more = kt + 1 < n_tiles;
+    if (more && ((kt + 1) * kTileBlocks) % kIdWin == 0) {
+      __syncthreads();
+      fill_ids((kt + 1) * kTileBlocks);
+    }
     __syncthreads();
-    if (kt + 1 < n_tiles) load_tile(j0 + kKeys);
+    if (more) load_tile(j0 + kKeys);
     if (!wave_active || j0 > wave_pos_max) continue;
 
-    // S^T = K Q^T for two 32-key halves of the tile.
-    f32x16 s[2];
+    // S^T = K Q^T for the two 32-key halves of the tile.
+    f32x16 s0, s1;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) { s[0][i] = 0.f; s[1][i] = 0.f; }
+    for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
+    bf16x8 ka = *(const bf16x8*)(sK + n * kRowBytes + ((hh ^ (n & 7)) << 4));
+    bf16x8 kb = *(const bf16x8*)(sK + (32 + n) * kRowBytes + ((hh ^ (n & 7)) << 4));
 #pragma unroll
     for (int kc = 0; kc < kDch; ++kc) {
-      const int c = kc * 2 + hh;
+      bf16x8 na = ka, nb = kb;
+      if (kc + 1 < kDch) {
+        const int c = (kc + 1) * 2 + hh;
+        na = *(const bf16x8*)(sK + n * kRowBytes + ((c ^ (n & 7)) << 4));
+        nb = *(const bf16x8*)(sK + (32 + n) * kRowBytes + ((c ^ (n & 7)) << 4));
+      }
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kc], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[kc], s1, 0, 0, 0);
+      ka = na;
+      kb = nb;
+    }
+
+    // Causal mask (only tiles that reach past some column's position).
+    if (j0 + kKeys - 1 > wave_pos_min) {
+      const int rel = pos - j0 - hh * 8;  // key (i>>3)*16 + (i&7) [+32] is visible iff <= rel
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const int row = st * 32 + n;
-        const bf16x8 a = *(const bf16x8*)(sK + row * kRowBytes + ((c ^ (row & 7)) << 4));
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kc], s[st], 0, 0, 0);
+      for (int i = 0; i < 16; ++i) {
+        const int k = (i >> 3) * 16 + (i & 7);
+        if (k > rel) s0[i] = -INFINITY;
+        if (k + 32 > rel) s1[i] = -INFINITY;
       }
     }
 
-    // Online softmax over this lane's column (log2 domain).
-    const bool need_mask = j0 + kKeys - 1 > wave_pos_min;
-    float x[32];
+    // Column max; O is rescaled only when it grew by more than 2^kLazyRescale.
+    float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
+    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
+    if (__ballot(mx > m_used + kLazyRescale)) {
+      const float m_new = fmaxf(m_used, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
+      m_used = m_new;
+      l_run *= alpha;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float v = s[st][i] * scale_log2;
-        if (need_mask) {
-          const int key = j0 + st * 32 + (i >> 3) * 16 + hh * 8 + (i & 7);
-          if (key > pos) v = -INFINITY;
-        }
-        x[st * 16 + i] = v;
-      }
-    float mloc = x[0];
+      for (int dt = 0; dt < kDt; ++dt)
 #pragma unroll
-    for (int i = 1; i < 32; ++i) mloc = fmaxf(mloc, x[i]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, mloc);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      x[i] = __builtin_amdgcn_exp2f(x[i] - m_new);
-      psum += x[i];
+        for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
     }
-    l_run = l_run * alpha + psum;
+
+    // P = exp2(S * scale_log2 - m_used) as bf16; the sum uses the same bf16 values.
+    bf16x8 pb[kTileBlocks];
 #pragma unroll
-    for (int dt = 0; dt < kDt; ++dt)
+    for (int i = 0; i < 16; ++i) {
+      pb[i >> 3][i & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[i], scale_log2, -m_used));
+      pb[2 + (i >> 3)][i & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[i], scale_log2, -m_used));
+    }
 #pragma unroll
-      for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
+    for (int b = 0; b < kTileBlocks; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 pr = {pb[b][2 * e], pb[b][2 * e + 1]};
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l_run, false);
+      }
 
     // O^T += V^T P^T, one 16-key pool block at a time.
 #pragma unroll
-    for (int kb = 0; kb < kTileBlocks; ++kb) {
-      bf16x8 pb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pb[e] = (__bf16)x[kb * 8 + e];
+    for (int b = 0; b < kTileBlocks; ++b)
 #pragma unroll
       for (int dt = 0; dt < kDt; ++dt) {
         const int d = dt * 32 + n;
         const bf16x8 a =
-            *(const bf16x8*)(sV + kb * kVBlockBytes + d * 32 + ((hh ^ ((d >> 2) & 1)) << 4));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[dt], 0, 0, 0);
+            *(const bf16x8*)(sV + b * kVBlockBytes + d * 32 + ((hh ^ ((d >> 2) & 1)) << 4));
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[b], o[dt], 0, 0, 0);
       }
-    }
   }
 
   if (!wave_active) return;
@@ -369,7 +413,7 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
   using ilpc::set_error;
   (void)workspace;
   (void)workspace_bytes;
-  if (B < 0 || max_q_len < 0 || num_blocks < 0 || max_blocks < 1 || Hq < 1 || Hkv < 1)
+  if (B < 0 || max_q_len < 0 || num_blocks < 1 || max_blocks < 1 || Hq < 1 || Hkv < 1)
     return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: negative or zero size");
   if (block_size != kBlock)
     return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: block_size must be 16");
@@ -385,18 +429,18 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
   if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
     return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: Q/K/V/out must be 16-byte aligned");
   const int64_t col_tiles = (int64_t(max_q_len) * (Hq / Hkv) + kCols - 1) / kCols;
-  if (B > 65535 || Hkv > 65535 || col_tiles > (int64_t(1) << 31) - 1)
+  const int64_t items = col_tiles * Hkv * B;
+  if (items > (int64_t(1) << 31) - 1)
     return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: grid too large");
   const float scale_log2 = softmax_scale * 1.4426950408889634f;
-  const dim3 grid(unsigned(col_tiles), Hkv, B);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (D == 128)
-    hipLaunchKernelGGL(paged_attn_kernel<128>, grid, dim3(kThreads), 0, s, q, k_pool, v_pool,
-                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv, scale_log2,
-                       out);
+    hipLaunchKernelGGL(paged_attn_kernel<128>, dim3(unsigned(items)), dim3(kThreads), 0, s, q, k_pool,
+                       v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv,
+                       int(col_tiles), scale_log2, out);
   else
-    hipLaunchKernelGGL(paged_attn_kernel<64>, grid, dim3(kThreads), 0, s, q, k_pool, v_pool,
-                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv, scale_log2,
-                       out);
+    hipLaunchKernelGGL(paged_attn_kernel<64>, dim3(unsigned(items)), dim3(kThreads), 0, s, q, k_pool,
+                       v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv,
+                       int(col_tiles), scale_log2, out);
   return launch_status("ilpc_paged_prefill_attn");
 }
