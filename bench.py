@@ -61,15 +61,21 @@ def kernel_source_sha() -> str:
 
 
 def traffic_from_profile(workload_name: str):
-    """Measured HBM bytes per launch from committed counter runs, if still current."""
-    path = os.path.join(ROOT, "profiles", f"paged_attn_{workload_name}_traffic.json")
+    """Measured HBM bytes per launch from the committed counter summary, or
+    None when there is none or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"paged_attn_{workload_name}_traffic.txt")
     if not os.path.exists(path):
         return None
+    fields = {}
     with open(path) as f:
-        d = json.load(f)
-    if d.get("kernel_source_sha") != kernel_source_sha():
-        return None  # kernel changed since the counters were taken
-    return d.get("hbm_bytes_per_launch")
+        for line in f:
+            if line.startswith("#") or ":" not in line:
+                continue
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    return float(fields["hbm_bytes_per_launch"]) if "hbm_bytes_per_launch" in fields else None
 
 
 def cpu_baseline(wl, cached_len, budget_s: float):

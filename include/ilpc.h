@@ -176,7 +176,8 @@ int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t 
  * sums in fp32 (matrix cores take bf16 operands), online softmax in fp32,
  * output rounded to bf16 (nearest-even).  A request with q_len_r > L_r, with
  * L_r > 16 * max_blocks, or whose blocks map outside [0, num_blocks) gets
- * unspecified output rows but causes no out-of-bounds access.
+ * unspecified output rows but causes no out-of-bounds access.  Block tables
+ * wider than 1024 blocks (contexts beyond 16384 tokens) are ILPC_EUNSUP.
  */
 int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
                             int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
