@@ -21,8 +21,8 @@
  *   - Arguments are validated before any state change or kernel launch.  A
  *     failing call leaves the cache unchanged; its outputs are unspecified.
  *   - Host pointers are marked [host], device pointers [device].  The caller
- *     owns every buffer; the library owns only the cache handle (host memory)
- *     and allocates no device memory.
+ *     owns every buffer (including the attention workspace); the library owns
+ *     only the cache handle (host memory) and allocates no device memory.
  *   - bf16 tensors are passed as uint16_t* holding the raw bf16 bits.
  *   - `stream` is a hipStream_t (NULL = the null stream).  Device calls are
  *     asynchronous on that stream; they return ILPC_EHIP when the launch
@@ -152,7 +152,7 @@ int ilpc_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_poo
                    int32_t max_new, int32_t Hkv, int32_t D, int32_t block_size, void* stream);
 
 /* Bytes of device workspace ilpc_paged_prefill_attn needs for these sizes
- * (currently always 0: the kernels keep all state on chip). */
+ * (currently 64 for every shape: the counters of its work queues). */
 int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
                               size_t* bytes);
 
@@ -169,7 +169,11 @@ int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t 
  * max_q_len    [host]   >= every q_len_r; rows beyond it are not computed
  * softmax_scale         multiplies q.k before the softmax (1/sqrt(D) usually)
  * out          [device] bf16 [cu_q[B], Hq, D]
- * workspace    [device] ilpc_attn_workspace_bytes() bytes, may be NULL if 0
+ * workspace    [device] >= ilpc_attn_workspace_bytes() bytes, 16-byte aligned,
+ *                      zero-filled before its first use.  Each call leaves it
+ *                      zero-filled again when its kernel completes, so calls
+ *                      ordered on one stream can share it; calls that may run
+ *                      concurrently (different streams) need separate ones.
  *
  * Query t of request r sits at position L_r - q_len_r + t and attends to keys
  * 0 .. L_r - q_len_r + t; q head h reads kv head h / (Hq/Hkv).  Products and
@@ -177,7 +181,8 @@ int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t 
  * output rounded to bf16 (nearest-even).  A request with q_len_r > L_r, with
  * L_r > 16 * max_blocks, or whose blocks map outside [0, num_blocks) gets
  * unspecified output rows but causes no out-of-bounds access.  Block tables
- * wider than 1024 blocks (contexts beyond 16384 tokens) are ILPC_EUNSUP.
+ * wider than 2^24 blocks are ILPC_EUNSUP; a missing or short workspace is
+ * ILPC_EINVAL.
  */
 int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
                             int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,

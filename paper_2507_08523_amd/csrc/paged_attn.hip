@@ -8,11 +8,12 @@
 //  * kv_append: scatter new K/V rows into 16-token pool blocks.  K blocks are
 //    token-major [16][D]; V blocks are stored dimension-major [D][16] so the
 //    attention kernel can feed them to the matrix cores without a transpose.
-//  * paged_attn: causal grouped-query attention of the suffix queries.  One
-//    workgroup (8 waves, one per CU) owns 256 query columns of one (request,
-//    kv head); a column is a (token, q head of the group) pair, so the G heads
-//    of a group share every K/V tile.  64-key tiles (4 pool blocks) stream
-//    through a 4-tile ring in LDS, filled by direct global-to-LDS loads three
+//  * paged_attn: causal grouped-query attention of the suffix queries.  A
+//    work item is 256 query columns of one (request, kv head); a column is a
+//    (token, q head of the group) pair, so the G heads of a group share every
+//    K/V tile.  The kernel is persistent (one 8-wave workgroup per CU) and
+//    takes items from per-XCD queues.  64-key tiles (4 pool blocks) stream
+//    through a 4-tile ring in LDS, filled by direct global-to-LDS loads two
 //    tiles ahead of use.  Per tile and wave:
 //      S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (a lane owns one column),
 //      causal mask, column max, online softmax in fp32 on exp2 with the scale
@@ -20,10 +21,13 @@
 //      O^T += V^T P^T on the same MFMA, P taken straight from the S^T
 //      accumulators (K rows are staged in a permuted order that makes the
 //      accumulator layout of S^T equal the operand layout P^T needs).
+//    The two waves sharing a SIMD run these steps half a tile apart, so one
+//    feeds the matrix core while the other computes the softmax.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "../../include/ilpc.h"
 #include "ilpc_internal.h"
@@ -155,17 +159,23 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// paged attention.  1-D grid over (column tile, kv head, request) work items,
-// heaviest column tile of a (request, kv head) first.  Work items are spread
-// so that those sharing one (request, kv head) -- and so the same K/V blocks --
-// land on the same XCD (workgroups are dealt round-robin to the 8 XCDs, each
-// with its own L2).
+// paged attention.  Work items are (column tile, kv head, request) triples,
+// numbered request-major with the heaviest column tile of a (request, kv head)
+// first.  The kernel is persistent: one workgroup per CU takes items from
+// eight queues, one per XCD, each holding a contiguous range of item numbers
+// so that the items sharing one (request, kv head) -- and so the same K/V
+// blocks -- are worked on under one XCD's L2.  A workgroup drains the queue
+// of its own XCD first, then helps the others.  The queue counters live in
+// the caller's workspace; the last workgroup to finish clears them again.
 //
 // K/V tiles stream through a ring of kStages tiles in LDS, filled straight
-// from HBM by global_load_lds kStages-1 tiles ahead of use; one barrier per
-// tile.  Each wave loads one pool block (its K rows and V rows) per tile.
-constexpr int kMaxTableBlocks = 1024;  // block-table width the kernel accepts (16384 tokens)
-constexpr float kLazyRescale = 8.f;    // log2 growth of a column max tolerated before rescaling O
+// from HBM by global_load_lds two tiles ahead of use.  Each wave loads one
+// pool block (its K rows and V rows) per tile; the block ids come from the
+// block table through scalar loads, one tile ahead of the load they steer.
+constexpr int kMaxTableBlocks = 1 << 24;  // block-table width accepted (keeps token positions in int)
+constexpr float kLazyRescale = 8.f;  // log2 growth of a column max tolerated before rescaling O
+constexpr int kQueueWords = 16;      // workspace: 8 queue counters, 1 finished-workgroup count
+constexpr int kDoneWord = 8;
 
 // s_waitcnt vmcnt(n) with the other counters left free (n < 16).
 template <int N>
@@ -173,6 +183,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 16, "vmcnt immediate");
   __builtin_amdgcn_s_waitcnt(0x0F70 | N);
 }
+
+// s_waitcnt lgkmcnt(0) with the other counters left free.
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // Workgroup barrier without the memory fence of __syncthreads: the caller
 // has already waited for exactly the loads it needs.  The empty asm keeps the
@@ -183,12 +196,19 @@ __device__ __forceinline__ void bare_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Index of the XCD (accelerator complex die) running this wave: hardware
+// register XCC_ID (id 20), bits 0-3.
+__device__ __forceinline__ unsigned xcd_id() {
+  return static_cast<unsigned>(__builtin_amdgcn_s_getreg((31 << 11) | 20)) & 7u;
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
     const uint16_t* __restrict__ v_pool, int num_blocks, const int32_t* __restrict__ block_tables,
     int max_blocks, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int Hq,
-    int Hkv, int n_col_tiles, float scale_log2, uint16_t* __restrict__ out) {
+    int Hkv, int n_col_tiles, unsigned n_items, float scale_log2, uint16_t* __restrict__ out,
+    unsigned* __restrict__ queue) {
   constexpr int kDch = D / 16;                    // 16-wide contraction chunks of Q.K^T
   constexpr int kDt = D / 32;                     // 32-row output tiles of O^T
   constexpr int kRowBytes = D * 2;                // one K row in LDS
@@ -202,233 +222,360 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   constexpr int kVInsts = kVTileBytes / 1024 / kWaves;
   constexpr int kLoads = kKInsts + kVInsts;
   static_assert(kKInsts >= 1 && kVInsts >= 1 && kWaves == 2 * kTileBlocks, "load split");
+  static_assert(kStages == 4, "ring: two tiles in flight plus two being read");
   __shared__ __attribute__((aligned(16))) uint8_t ring[kStages * kStageBytes];
-  __shared__ __attribute__((aligned(16))) int32_t s_ids[kMaxTableBlocks + kTileBlocks];
-
-  // XCD-aware decode of the work item.
-  const unsigned n_items = gridDim.x, bid = blockIdx.x;
-  const unsigned xcd = bid & 7u, per = n_items >> 3, extra = n_items & 7u;
-  const unsigned w = xcd * per + min(xcd, extra) + (bid >> 3);
-  const int tile = n_col_tiles - 1 - int(w % unsigned(n_col_tiles));
-  const unsigned rest = w / unsigned(n_col_tiles);
-  const int kvh = int(rest % unsigned(Hkv));
-  const int r = int(rest / unsigned(Hkv));
-
-  const int G = Hq / Hkv;
-  const int q0 = cu_q[r];
-  const int q_len = cu_q[r + 1] - q0;
-  const int n_cols = q_len * G;
-  const int col0 = tile * kCols;
-  int L = seq_lens[r];
-  if (L > max_blocks * kBlock) L = max_blocks * kBlock;
-  if (q_len <= 0 || col0 >= n_cols || q_len > L) return;
+  __shared__ int s_item[2];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int n = lane & 31, hh = lane >> 5;
-  const int qstart = L - q_len;  // position of the request's first query
+  const int G = Hq / Hkv;
+  const size_t slab_stride = size_t(Hkv) * kSlabBytes;
 
-  // This lane's query column (padding columns repeat the last valid one).
-  const int col = col0 + wave * kColsPerWave + n;
-  const bool col_valid = col < n_cols;
-  const int colc = col_valid ? col : n_cols - 1;
-  const int t = colc / G;
-  const int pos = qstart + t;
-  const size_t qrow = (size_t(q0 + t) * Hq + size_t(kvh) * G + (colc - t * G)) * D;
-
-  const int wave_first = col0 + wave * kColsPerWave;
-  const bool wave_active = wave_first < n_cols;
-  const int wave_pos_min = qstart + min(wave_first, n_cols - 1) / G;
-  const int wave_pos_max = wave_active ? qstart + min(wave_first + kColsPerWave - 1, n_cols - 1) / G : -1;
-  const int wg_pos_max = qstart + min(col0 + kCols - 1, n_cols - 1) / G;
-  const int n_tiles = wg_pos_max / kKeys + 1;
-  const int n_blk_used = (wg_pos_max >> 4) + 1;  // <= ceil(L / 16) <= max_blocks
-  const int key_lim = wg_pos_max + 1;            // keys at or past this are masked everywhere
-
-  bf16x8 qf[kDch];
-#pragma unroll
-  for (int kc = 0; kc < kDch; ++kc) qf[kc] = as_bf16x8(*(const u32x4*)(q + qrow + kc * 16 + hh * 8));
-  // Q is in before any tile load is issued, so the waits in the tile loop can
-  // count tile loads only.
-  wait_vmcnt<0>();
-  asm volatile("" ::: "memory");
-
-  // Block ids -> LDS; unusable ids read block 0 instead (stray K rows only
-  // meet masked scores, stray V rows past key_lim are zeroed below).
-  const int32_t* bt = block_tables + size_t(r) * max_blocks;
-  for (int i = tid; i < kMaxTableBlocks + kTileBlocks; i += kThreads) {
-    int id = 0;
-    if (i < n_blk_used) {
-      id = bt[i];
-      if (id < 0 || id >= num_blocks) id = 0;
+  // Item queues.  Queue x holds items [x*per + min(x, extra), ...) of
+  // per + (x < extra) items; fetch() (lane 0 of wave 0 only) returns the next
+  // item, or -1 once every queue is drained.
+  const unsigned home = xcd_id(), per = n_items >> 3, extra = n_items & 7u;
+  unsigned qsel = 0;
+  auto fetch = [&]() -> int {
+    while (qsel < 8u) {
+      const unsigned x = (home + qsel) & 7u;
+      const unsigned size = per + (x < extra ? 1u : 0u), base = x * per + min(x, extra);
+      const unsigned i = __hip_atomic_fetch_add(queue + x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (i < size) return int(base + i);
+      ++qsel;
     }
-    s_ids[i] = id;
-  }
+    return -1;
+  };
 
   // This wave's direct loads of a tile: all from pool block wave/2 of the tile.
   // LDS slot (row m, slot p) of a K tile holds chunk k_slot(m, p) of key
   // key_row(m); slot (d, p) of a V block holds half v_slot(d, p) of row d.
   uint32_t koff[kKInsts], voff[kVInsts];
 #pragma unroll
-  for (int it = 0; it < kKInsts; ++it) {
-    const int g = wave * kKInsts + it;
+  for (int i = 0; i < kKInsts; ++i) {
+    const int g = wave * kKInsts + i;
     const int m = g * (1024 / kRowBytes) + lane / kKch;
-    koff[it] = uint32_t((key_row(m) & 15) * kRowBytes + k_slot<D>(m, lane % kKch) * 16);
+    koff[i] = uint32_t((key_row(m) & 15) * kRowBytes + k_slot<D>(m, lane % kKch) * 16);
   }
 #pragma unroll
-  for (int it = 0; it < kVInsts; ++it) {
-    const int g = wave * kVInsts + it;
+  for (int i = 0; i < kVInsts; ++i) {
+    const int g = wave * kVInsts + i;
     const int d = (g * 1024 % kVBlockBytes) / 32 + (lane >> 1);
-    voff[it] = uint32_t(d * 32 + v_slot(d, lane & 1) * 16);
+    voff[i] = uint32_t(d * 32 + v_slot(d, lane & 1) * 16);
   }
   const int my_blk = wave >> 1;
-  const uint8_t* kbase = reinterpret_cast<const uint8_t*>(k_pool) + size_t(kvh) * kSlabBytes;
-  const uint8_t* vbase = reinterpret_cast<const uint8_t*>(v_pool) + size_t(kvh) * kSlabBytes;
-  const size_t slab_stride = size_t(Hkv) * kSlabBytes;
-
-  auto issue_tile = [&](int tl) {
-    const int id = __builtin_amdgcn_readfirstlane(s_ids[tl * kTileBlocks + my_blk]);
-    uint8_t* st = ring + (tl % kStages) * kStageBytes;
-    const uint8_t* ksrc = kbase + size_t(id) * slab_stride;
-    const uint8_t* vsrc = vbase + size_t(id) * slab_stride;
-#pragma unroll
-    for (int it = 0; it < kKInsts; ++it) global_to_lds16(ksrc + koff[it], st + (wave * kKInsts + it) * 1024);
-#pragma unroll
-    for (int it = 0; it < kVInsts; ++it)
-      global_to_lds16(vsrc + voff[it], st + kKTileBytes + (wave * kVInsts + it) * 1024);
-  };
-  // Zero the V rows of keys >= key_lim in a V tile (only the tile crossing it).
-  auto zero_v_tail = [&](int j0, uint8_t* sV) {
-    for (int slot = tid; slot < kVTileBytes / 16; slot += kThreads) {
-      const int kb = slot / (2 * D), d = (slot % (2 * D)) >> 1, p = slot & 1;
-      const int nvalid = key_lim - (j0 + kb * kBlock + v_slot(d, p) * 8);
-      if (nvalid < 8) {
-        u32x4* ptr = (u32x4*)(sV + kb * kVBlockBytes + d * 32 + p * 16);
-        u32x4 v = *ptr;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          v[e] &= (2 * e < nvalid ? 0x0000FFFFu : 0u) | (2 * e + 1 < nvalid ? 0xFFFF0000u : 0u);
-        *ptr = v;
-      }
-    }
-  };
-
-  f32x16 o[kDt];
-#pragma unroll
-  for (int dt = 0; dt < kDt; ++dt)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) o[dt][i] = 0.f;
-  float m_used = -INFINITY;  // max (log2 units) the exponentials of this column are taken against
-  float l_run = 0.f;         // this lane half's share of the column's exponential sum
+  const bool lag = wave >= kWaves / 2;
   const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
 
-  __syncthreads();  // block ids visible
-#pragma unroll
-  for (int tl = 0; tl < kStages - 1; ++tl)
-    if (tl < n_tiles) issue_tile(tl);
+  if (tid == 0) {
+    s_item[0] = fetch();
+    wait_lgkmcnt0();
+  }
+  __syncthreads();
 
-  for (int i = 0; i < n_tiles; ++i) {
-    const int j0 = i * kKeys;
-    // this wave's loads of tile i have landed (later tiles may stay in flight)
-    const int ahead = min(kStages - 2, n_tiles - 1 - i);
-    if (ahead >= 2) wait_vmcnt<2 * kLoads>();
-    else if (ahead == 1) wait_vmcnt<kLoads>();
-    else wait_vmcnt<0>();
-    bare_barrier();  // every wave's loads of tile i are in; tile i-1's stage is free
-    uint8_t* const sK = ring + (i % kStages) * kStageBytes;
-    uint8_t* const sV = sK + kKTileBytes;
-    if (j0 + kKeys > key_lim) {
-      zero_v_tail(j0, sV);
+  // Ring stages are numbered by a tile count running across items, so the
+  // first tiles of an item never land in the stage the previous item still
+  // reads.
+  int tbase = 0;
+  for (int it = 0;; ++it) {
+    const int w = __builtin_amdgcn_readfirstlane(s_item[it & 1]);
+    if (w < 0) break;
+    const int tile = n_col_tiles - 1 - int(unsigned(w) % unsigned(n_col_tiles));
+    const unsigned rest = unsigned(w) / unsigned(n_col_tiles);
+    const int kvh = int(rest % unsigned(Hkv));
+    const int r = int(rest / unsigned(Hkv));
+    const int q0 = cu_q[r];
+    const int q_len = cu_q[r + 1] - q0;
+    const int n_cols = q_len * G;
+    const int col0 = tile * kCols;
+    int L = seq_lens[r];
+    if (L > max_blocks * kBlock) L = max_blocks * kBlock;
+    if (q_len <= 0 || col0 >= n_cols || q_len > L) {  // nothing to do for this item
+      if (tid == 0) {
+        s_item[(it + 1) & 1] = fetch();
+        wait_lgkmcnt0();
+      }
       __syncthreads();
+      continue;
     }
-    if (i + kStages - 1 < n_tiles) issue_tile(i + kStages - 1);
-    if (j0 > wave_pos_max) continue;
+    const int qstart = L - q_len;  // position of the request's first query
 
-    // S^T = K Q^T for the two 32-key halves of the tile.
-    f32x16 s0, s1;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) { s0[e] = 0.f; s1[e] = 0.f; }
-#pragma unroll
-    for (int kc = 0; kc < kDch; ++kc) {
-      const int c = kc * 2 + hh;
-      const bf16x8 a0 = *(const bf16x8*)(sK + n * kRowBytes + (k_slot<D>(n, c) << 4));
-      const bf16x8 a1 = *(const bf16x8*)(sK + (32 + n) * kRowBytes + (k_slot<D>(32 + n, c) << 4));
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[kc], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[kc], s1, 0, 0, 0);
-    }
+    // This lane's query column (padding columns repeat the last valid one).
+    const int col = col0 + wave * kColsPerWave + n;
+    const bool col_valid = col < n_cols;
+    const int colc = col_valid ? col : n_cols - 1;
+    const int t = colc / G;
+    const int pos = qstart + t;
+    const size_t qrow = (size_t(q0 + t) * Hq + size_t(kvh) * G + (colc - t * G)) * D;
 
-    // Causal mask (only tiles that reach past some column's position).
-    if (j0 + kKeys - 1 > wave_pos_min) {
-      const int rel = pos - j0 - hh * 8;  // key (e>>3)*16 + (e&7) [+32] is visible iff <= rel
+    const int wave_first = col0 + wave * kColsPerWave;
+    const bool wave_active = wave_first < n_cols;
+    const int wave_pos_min = qstart + min(wave_first, n_cols - 1) / G;
+    const int wg_pos_max = qstart + min(col0 + kCols - 1, n_cols - 1) / G;
+    const int n_tiles = wg_pos_max / kKeys + 1;
+    const int n_blk_used = (wg_pos_max >> 4) + 1;  // <= ceil(L / 16) <= max_blocks
+    const int key_lim = wg_pos_max + 1;            // keys at or past this are masked everywhere
+
+    bf16x8 qf[kDch];
+#pragma unroll
+    for (int kc = 0; kc < kDch; ++kc) qf[kc] = as_bf16x8(*(const u32x4*)(q + qrow + kc * 16 + hh * 8));
+
+    const int32_t* bt = block_tables + size_t(r) * max_blocks;
+    const uint8_t* kbase = reinterpret_cast<const uint8_t*>(k_pool) + size_t(kvh) * kSlabBytes;
+    const uint8_t* vbase = reinterpret_cast<const uint8_t*>(v_pool) + size_t(kvh) * kSlabBytes;
+    // Pool block of this wave in tile tl; unusable ids read block 0 instead
+    // (stray K rows only meet masked scores, stray V rows past key_lim are
+    // zeroed below).  A wave-uniform index: a scalar load.
+    auto block_id = [&](int tl) -> int {
+      const int i = tl * kTileBlocks + my_blk;
+      int id = i < n_blk_used ? bt[i] : 0;
+      return (id < 0 || id >= num_blocks) ? 0 : id;
+    };
+    auto stage = [&](int tl) { return ring + ((tbase + tl) % kStages) * kStageBytes; };
+    int id_next = block_id(0);
+    auto issue_tile = [&](int tl) {  // tiles are issued in order 0, 1, 2, ...
+      const int id = id_next;
+      id_next = block_id(tl + 1);
+      uint8_t* st = stage(tl);
+      const uint8_t* ksrc = kbase + size_t(id) * slab_stride;
+      const uint8_t* vsrc = vbase + size_t(id) * slab_stride;
+#pragma unroll
+      for (int i = 0; i < kKInsts; ++i) global_to_lds16(ksrc + koff[i], st + (wave * kKInsts + i) * 1024);
+#pragma unroll
+      for (int i = 0; i < kVInsts; ++i)
+        global_to_lds16(vsrc + voff[i], st + kKTileBytes + (wave * kVInsts + i) * 1024);
+    };
+    // Zero the V rows of keys >= key_lim in a V tile (only the tile crossing it).
+    auto zero_v_tail = [&](int j0, uint8_t* sV) {
+      for (int slot = tid; slot < kVTileBytes / 16; slot += kThreads) {
+        const int kb = slot / (2 * D), d = (slot % (2 * D)) >> 1, p = slot & 1;
+        const int nvalid = key_lim - (j0 + kb * kBlock + v_slot(d, p) * 8);
+        if (nvalid < 8) {
+          u32x4* ptr = (u32x4*)(sV + kb * kVBlockBytes + d * 32 + p * 16);
+          u32x4 v = *ptr;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[e] &= (2 * e < nvalid ? 0x0000FFFFu : 0u) | (2 * e + 1 < nvalid ? 0xFFFF0000u : 0u);
+          *ptr = v;
+        }
+      }
+    };
+
+    f32x16 o[kDt];
+#pragma unroll
+    for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[dt][i] = 0.f;
+    float m_used = -INFINITY;  // max (log2 units) the exponentials of this column are taken against
+    float l_run = 0.f;         // this lane half's share of the column's exponential sum
+    bf16x8 pb[kTileBlocks];    // P of the tile whose V^T P^T is still due
+    f32x16 sc0, sc1;           // scores of the tile whose softmax is next
+
+    // Softmax step of the score tile starting at key j0: causal mask, column
+    // max, lazy rescale of O, P = exp2(S * scale_log2 - m) as bf16 (the sum
+    // uses the same bf16 values).
+    auto softmax = [&](int j0) {
+      if (j0 + kKeys - 1 > wave_pos_min) {
+        const int rel = pos - j0 - hh * 8;  // key (e>>3)*16 + (e&7) [+32] is visible iff <= rel
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int k = (e >> 3) * 16 + (e & 7);
+          sc0[e] = k > rel ? -INFINITY : sc0[e];
+          sc1[e] = k + 32 > rel ? -INFINITY : sc1[e];
+        }
+      }
+      float mx = max3f(sc0[0], sc1[0], sc0[1]);
+      mx = max3f(mx, sc1[1], sc0[2]);
+#pragma unroll
+      for (int e = 2; e < 15; ++e) mx = max3f(mx, sc1[e], sc0[e + 1]);
+      mx = max3f(mx, sc1[15], mx);
+      mx = max_across_halves(mx) * scale_log2;
+      if (__ballot(mx > m_used + kLazyRescale)) {
+        const float m_new = fmaxf(m_used, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
+        m_used = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+      }
+      float ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int k = (e >> 3) * 16 + (e & 7);
-        s0[e] = k > rel ? -INFINITY : s0[e];
-        s1[e] = k + 32 > rel ? -INFINITY : s1[e];
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc0[e], scale_log2, -m_used));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc1[e], scale_log2, -m_used));
+        pb[e >> 3][e & 7] = (__bf16)p0;
+        pb[2 + (e >> 3)][e & 7] = (__bf16)p1;
+        ls[e & 3] += p0 + p1;
+      }
+      l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    };
+
+    // One matrix-core phase: O += V(sV) P over the tile's pool blocks
+    // (kTileBlocks * kDt products), then S = K(sK) Q^T (2 * kDch products),
+    // as one software-pipelined stream whose LDS operands are read kPrefetch
+    // products ahead, so that a lone wave keeps the matrix core busy.
+    constexpr int kPvSteps = kTileBlocks * kDt, kQkSteps = 2 * kDch, kPrefetch = 4;
+    auto m_phase = [&](auto with_pv, auto with_qk, const uint8_t* sV, const uint8_t* sK) {
+      constexpr int first = decltype(with_pv)::value ? 0 : kPvSteps;
+      constexpr int last = decltype(with_qk)::value ? kPvSteps + kQkSteps : kPvSteps;
+      auto operand = [&](int st) -> bf16x8 {
+        if (st < kPvSteps) {
+          const int b = st / kDt, d = (st % kDt) * 32 + n;
+          return *(const bf16x8*)(sV + b * kVBlockBytes + d * 32 + (v_slot(d, hh) << 4));
+        }
+        const int u = st - kPvSteps, m = (u & 1) * 32 + n;
+        return *(const bf16x8*)(sK + m * kRowBytes + (k_slot<D>(m, (u >> 1) * 2 + hh) << 4));
+      };
+      if constexpr (decltype(with_qk)::value) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) { sc0[e] = 0.f; sc1[e] = 0.f; }
+      }
+      bf16x8 buf[kPrefetch];
+#pragma unroll
+      for (int st = first; st < first + kPrefetch && st < last; ++st) buf[st % kPrefetch] = operand(st);
+#pragma unroll
+      for (int st = first; st < last; ++st) {
+        const bf16x8 a = buf[st % kPrefetch];
+        if (st + kPrefetch < last) buf[st % kPrefetch] = operand(st + kPrefetch);
+        if (st < kPvSteps) {
+          const int dt = st % kDt;
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[st / kDt], o[dt], 0, 0, 0);
+        } else {
+          const int u = st - kPvSteps;
+          if (u & 1) sc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[u >> 1], sc1, 0, 0, 0);
+          else sc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[u >> 1], sc0, 0, 0, 0);
+        }
+      }
+      // Pin the pipelined order for the scheduler (mask 0x100: LDS reads,
+      // 0x008: matrix-core ops): kPrefetch reads, then one product per read,
+      // then the last kPrefetch products.
+      constexpr int steps = last - first, lead = steps < kPrefetch ? steps : kPrefetch;
+      __builtin_amdgcn_sched_group_barrier(0x100, lead, 0);
+#pragma unroll
+      for (int st = 0; st < steps - lead; ++st) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, lead, 0);
+    };
+    using yes = std::true_type;
+    using no = std::false_type;
+
+    // Ping-pong schedule.  Every wave runs the same phase sequence
+    //   M_0 = [S(0) = K(0) Q^T]
+    //   V_0 = [softmax S(0) -> P(0)]
+    //   M_j = [O += V(j-1) P(j-1); S(j) = K(j) Q^T]   j = 1 .. n_tiles-1
+    //   V_j = [softmax S(j) -> P(j)]
+    //   M_n = [O += V(n-1) P(n-1)]
+    // with a workgroup barrier before every phase.  Waves kWaves/2 .. kWaves-1
+    // pass one extra barrier first (and waves 0 .. kWaves/2-1 one at the
+    // end), so the second half runs one phase behind the first: while one
+    // wave of a SIMD issues matrix-core work (M) its partner runs the vector
+    // softmax (V).
+    //
+    // Counting this item's barriers, the first half runs phase number p (M_j
+    // is p = 2j, V_j is p = 2j+1) after barrier p and the second half after
+    // barrier p+1.  Hence:
+    //   - every wave waits for its own loads of tile j before the barrier
+    //     that opens V_{j-1}: barrier 2j-1 or 2j, so all of tile j is in LDS
+    //     by barrier 2j, where the first half starts M_j;
+    //   - the V tail of tile j is zeroed at the start of M_j (after barrier
+    //     2j or 2j+1, once tile j is complete) and read in M_{j+1} (after
+    //     barrier 2j+2 or 2j+3);
+    //   - tile j+2 is issued at the start of M_j, into the stage of tile j-2,
+    //     whose last reader M_{j-1} ended by barrier 2j everywhere.
+    // The ring thus holds tiles j-1 (V still due), j, j+1 (in flight) and
+    // j+2.  Across items the stage count runs on: when the first half starts
+    // the next item, the second half may still be in M_n of this one, which
+    // reads the stage of tile n-1, while the next item's tiles 0, 1 and 2 go
+    // to the stages after it.
+    auto wait_tile = [&](int j) {  // this wave's loads of tile j are in (j + 1 may be in flight)
+      if (j + 1 < n_tiles) wait_vmcnt<kLoads>();
+      else wait_vmcnt<0>();
+    };
+    auto begin_m = [&](int j) {
+      bare_barrier();
+      if (j < n_tiles && j * kKeys + kKeys > key_lim) {
+        zero_v_tail(j * kKeys, stage(j) + kKTileBytes);
+        wait_lgkmcnt0();  // zeros in LDS before the next barrier
+      }
+      if (j + 2 < n_tiles) issue_tile(j + 2);
+    };
+
+    issue_tile(0);
+    if (1 < n_tiles) issue_tile(1);
+    if (tid == 0) {  // the next item, fetched while the first tiles load
+      s_item[(it + 1) & 1] = fetch();
+      wait_lgkmcnt0();
+    }
+    // Q and tiles 0 and 1 in (before the second half's extra barrier, which
+    // stands in for the barrier opening V_{-1}).
+    wait_vmcnt<0>();
+    if (lag) bare_barrier();
+    begin_m(0);
+    if (wave_active) m_phase(no(), yes(), nullptr, stage(0));
+    if (n_tiles > 1) wait_tile(1);
+    bare_barrier();
+    if (wave_active) softmax(0);
+    for (int j = 1; j < n_tiles; ++j) {
+      begin_m(j);
+      if (wave_active) m_phase(yes(), yes(), stage(j - 1) + kKTileBytes, stage(j));
+      if (j + 1 < n_tiles) wait_tile(j + 1);
+      bare_barrier();
+      if (wave_active) softmax(j * kKeys);
+    }
+    begin_m(n_tiles);
+    if (wave_active) m_phase(yes(), no(), stage(n_tiles - 1) + kKTileBytes, nullptr);
+    if (!lag) bare_barrier();
+    tbase += n_tiles;
+
+    if (wave_active) {
+      const float l_tot = l_run + __shfl_xor(l_run, 32);
+      const float inv = 1.f / l_tot;
+      if (col_valid) {
+        uint16_t* orow = out + qrow;
+#pragma unroll
+        for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            bf16x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = (__bf16)(o[dt][g4 * 4 + e] * inv);
+            *(bf16x4*)(orow + dt * 32 + g4 * 8 + hh * 4) = v;
+          }
       }
     }
-
-    // Column max; O is rescaled only when it grew by more than 2^kLazyRescale.
-    float mx = max3f(s0[0], s1[0], s0[1]);
-    mx = max3f(mx, s1[1], s0[2]);
-#pragma unroll
-    for (int e = 2; e < 15; ++e) mx = max3f(mx, s1[e], s0[e + 1]);
-    mx = max3f(mx, s1[15], mx);
-    mx = max_across_halves(mx) * scale_log2;
-    if (__ballot(mx > m_used + kLazyRescale)) {
-      const float m_new = fmaxf(m_used, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
-      m_used = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < kDt; ++dt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
-    }
-
-    // P = exp2(S * scale_log2 - m_used) as bf16; the sum uses the same bf16 values.
-    bf16x8 pb[kTileBlocks];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      pb[e >> 3][e & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s0[e], scale_log2, -m_used));
-      pb[2 + (e >> 3)][e & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s1[e], scale_log2, -m_used));
-    }
-#pragma unroll
-    for (int b = 0; b < kTileBlocks; ++b)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bf16x2 pr = {pb[b][2 * e], pb[b][2 * e + 1]};
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l_run, false);
-      }
-
-    // O^T += V^T P^T, one 16-key pool block at a time.
-#pragma unroll
-    for (int b = 0; b < kTileBlocks; ++b)
-#pragma unroll
-      for (int dt = 0; dt < kDt; ++dt) {
-        const int d = dt * 32 + n;
-        const bf16x8 a = *(const bf16x8*)(sV + b * kVBlockBytes + d * 32 + (v_slot(d, hh) << 4));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[b], o[dt], 0, 0, 0);
-      }
   }
 
-  if (!wave_active) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv = 1.f / l_tot;
-  if (!col_valid) return;
-  uint16_t* orow = out + qrow;
-#pragma unroll
-  for (int dt = 0; dt < kDt; ++dt)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      bf16x4 v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (__bf16)(o[dt][g4 * 4 + e] * inv);
-      *(bf16x4*)(orow + dt * 32 + g4 * 8 + hh * 4) = v;
+  // Every queue is drained.  The last workgroup out clears the counters for
+  // the next call on this workspace (no workgroup fetches any more by then).
+  if (tid == 0) {
+    const unsigned done =
+        __hip_atomic_fetch_add(queue + kDoneWord, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (done == gridDim.x - 1) {
+      for (int i = 0; i <= kDoneWord; ++i)
+        __hip_atomic_store(queue + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+  }
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Compute units of the current device (one persistent workgroup each),
+// looked up once per device.
+int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (dev < 64) cached[dev] = cus;
+  return cus;
+}
 
 int launch_status(const char* what) {
   const hipError_t e = hipGetLastError();
@@ -471,7 +618,7 @@ extern "C" int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t H
                                          int32_t D, size_t* bytes) {
   if (!bytes || B < 0 || max_q_len < 0 || Hq < 1 || Hkv < 1 || D < 1)
     return ilpc::set_error(ILPC_EINVAL, "ilpc_attn_workspace_bytes: bad argument");
-  *bytes = 0;
+  *bytes = kQueueWords * sizeof(unsigned);
   return ILPC_OK;
 }
 
@@ -483,8 +630,6 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
                                        int32_t block_size, float softmax_scale, uint16_t* out,
                                        void* workspace, size_t workspace_bytes, void* stream) {
   using ilpc::set_error;
-  (void)workspace;
-  (void)workspace_bytes;
   if (B < 0 || max_q_len < 0 || num_blocks < 1 || max_blocks < 1 || Hq < 1 || Hkv < 1)
     return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: negative or zero size");
   if (block_size != kBlock)
@@ -496,26 +641,32 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
   if (!std::isfinite(softmax_scale))
     return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: softmax_scale is not finite");
   if (max_blocks > kMaxTableBlocks)
-    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: max_blocks %d > %d (contexts up to %d tokens)",
-                     max_blocks, kMaxTableBlocks, kMaxTableBlocks * kBlock);
+    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: max_blocks %d > %d", max_blocks, kMaxTableBlocks);
   if (B == 0 || max_q_len == 0) return ILPC_OK;
   if (!q || !k_pool || !v_pool || !block_tables || !cu_q || !seq_lens || !out)
     return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: NULL pointer");
   if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
     return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: Q/K/V/out must be 16-byte aligned");
+  if (!workspace || workspace_bytes < kQueueWords * sizeof(unsigned) || !aligned16(workspace))
+    return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: workspace must be %zu bytes, 16-byte aligned",
+                     kQueueWords * sizeof(unsigned));
   const int64_t col_tiles = (int64_t(max_q_len) * (Hq / Hkv) + kCols - 1) / kCols;
   const int64_t items = col_tiles * Hkv * B;
   if (items > (int64_t(1) << 31) - 1)
     return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: grid too large");
   const float scale_log2 = softmax_scale * 1.4426950408889634f;
+  const int cus = device_cus();
+  if (cus <= 0) return set_error(ILPC_EHIP, "ilpc_paged_prefill_attn: cannot query the device");
+  const unsigned grid = unsigned(items < cus ? items : cus);
+  unsigned* queue = static_cast<unsigned*>(workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (D == 128)
-    hipLaunchKernelGGL(paged_attn_kernel<128>, dim3(unsigned(items)), dim3(kThreads), 0, s, q, k_pool,
-                       v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv,
-                       int(col_tiles), scale_log2, out);
+    hipLaunchKernelGGL(paged_attn_kernel<128>, dim3(grid), dim3(kThreads), 0, s, q, k_pool, v_pool,
+                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv, int(col_tiles),
+                       unsigned(items), scale_log2, out, queue);
   else
-    hipLaunchKernelGGL(paged_attn_kernel<64>, dim3(unsigned(items)), dim3(kThreads), 0, s, q, k_pool,
-                       v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv,
-                       int(col_tiles), scale_log2, out);
+    hipLaunchKernelGGL(paged_attn_kernel<64>, dim3(grid), dim3(kThreads), 0, s, q, k_pool, v_pool,
+                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv, int(col_tiles),
+                       unsigned(items), scale_log2, out, queue);
   return launch_status("ilpc_paged_prefill_attn");
 }

@@ -192,9 +192,35 @@ def attn_workspace_bytes(B, max_q_len, Hq, Hkv, D) -> int:
     return int(n.value)
 
 
+_workspaces = {}
+
+
+def attn_workspace(device=None, stream=None):
+    """A zero-filled attention workspace kept for one (device, stream) pair.
+
+    The attention call leaves its workspace zero-filled again, so one buffer
+    serves every call issued on that stream; calls on different streams get
+    different buffers because concurrent calls must not share one.
+    """
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    key = (stream.device.index, stream.cuda_stream)
+    ws = _workspaces.get(key)
+    if ws is None:
+        ws = torch.zeros(attn_workspace_bytes(0, 0, 1, 1, 1), dtype=torch.uint8, device=stream.device)
+        _workspaces[key] = ws
+    return ws
+
+
 def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_len: int, scale: float,
                        out, workspace=None, stream=None):
-    """Causal GQA attention of packed queries [total, Hq, D] over the paged pools."""
+    """Causal GQA attention of packed queries [total, Hq, D] over the paged pools.
+
+    `workspace` defaults to the zero-filled buffer attn_workspace() keeps for
+    the stream the call is issued on.
+    """
     import torch
 
     NB, Hkv, bs, D = k_pool.shape
@@ -204,9 +230,9 @@ def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_le
         raise ILPCError(EINVAL, "paged_prefill_attn: inconsistent Q/K/V/out shapes")
     if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
         raise ILPCError(EINVAL, "paged_prefill_attn: inconsistent batch shapes")
-    ws_ptr, ws_bytes = None, 0
-    if workspace is not None:
-        ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace", 1), workspace.numel()
+    if workspace is None:
+        workspace = attn_workspace(q.device, stream)
+    ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace", 1), workspace.numel()
     args = (_dev(q, torch.bfloat16, "q", 3), _dev(k_pool, torch.bfloat16, "k_pool", 4),
             _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
             _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],

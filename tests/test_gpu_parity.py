@@ -267,14 +267,47 @@ def test_abi_rejects_bad_arguments_on_device():
     b, pc, q = run.batch, run.pc, run.rows["q"]
     lib = ilpc.load()
 
-    def call(q_ptr, Hq, Hkv, D):
+    ws = torch.zeros(64, dtype=torch.uint8, device="cuda")
+
+    def call(q_ptr, Hq, Hkv, D, ws_ptr=None, ws_bytes=0):
         return lib.ilpc_paged_prefill_attn(q_ptr, pc.k_pool.data_ptr(), pc.v_pool.data_ptr(),
                                            pc.num_blocks, b.block_tables.data_ptr(), pc.max_blocks,
                                            b.cu_q.data_ptr(), b.seq_lens.data_ptr(), b.B, b.max_q_len,
-                                           Hq, Hkv, D, 16, 0.125, run.out.data_ptr(), None, 0, None)
+                                           Hq, Hkv, D, 16, 0.125, run.out.data_ptr(), ws_ptr, ws_bytes, None)
 
     assert call(q.data_ptr(), 4, 1, 96) == ilpc.EUNSUP       # head_dim
     assert call(q.data_ptr() + 2, 4, 1, 64) == ilpc.EINVAL   # misaligned Q
     assert call(q.data_ptr(), 6, 4, 64) == ilpc.EUNSUP       # Hq % Hkv != 0
     assert call(None, 4, 1, 64) == ilpc.EINVAL               # NULL
+    assert call(q.data_ptr(), 4, 1, 64) == ilpc.EINVAL       # no workspace
+    assert call(q.data_ptr(), 4, 1, 64, ws.data_ptr(), 32) == ilpc.EINVAL       # short workspace
+    assert call(q.data_ptr(), 4, 1, 64, ws.data_ptr() + 4, 60) == ilpc.EINVAL   # misaligned workspace
     assert lib.ilpc_last_error().decode()
+
+
+def test_work_queue_workspace_reused_and_left_zeroed():
+    # The persistent attention kernel hands out work items from counters in the
+    # workspace and the last workgroup clears them: back-to-back calls on one
+    # workspace, and calls on a second stream with their own workspace, give
+    # identical outputs and leave every workspace zero-filled.
+    run = Run("qwen7b")
+    b, pc, q, scale = run.batch, run.pc, run.rows["q"], run.wl.spec.scale
+    ws = torch.zeros(ilpc.attn_workspace_bytes(b.B, b.max_q_len, 28, 4, 128), dtype=torch.uint8, device="cuda")
+    outs = []
+    for _ in range(3):
+        out = torch.empty_like(q)
+        ilpc.paged_prefill_attn(q, pc.k_pool, pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, b.max_q_len,
+                                scale, out, ws)
+        outs.append(out)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        out = torch.empty_like(q)
+        ilpc.paged_prefill_attn(q, pc.k_pool, pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, b.max_q_len,
+                                scale, out, None, side)
+        outs.append(out)
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
+    assert int(ws.count_nonzero()) == 0
+    assert int(ilpc.attn_workspace(None, side).count_nonzero()) == 0

@@ -189,3 +189,12 @@ def test_keys_are_never_zero_and_chain(lib):
     _, _, k = ilpc.PrefixCache(64, 8).match([toks], want_keys=True)
     assert [int(x) for x in k[0, :5]] == chain_keys(toks)
     assert (k[0, :5] != 0).all() and (k[0, 5:] == 0).all()
+
+
+def test_attn_workspace_bytes_host_only():
+    # the workspace query touches no device: the size of the work-queue counters
+    assert ilpc.attn_workspace_bytes(4, 128, 32, 8, 128) == 64
+    assert ilpc.attn_workspace_bytes(0, 0, 1, 1, 64) == 64
+    with pytest.raises(ilpc.ILPCError) as e:
+        ilpc.attn_workspace_bytes(-1, 0, 1, 1, 64)
+    assert e.value.code == ilpc.EINVAL
