@@ -285,12 +285,22 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const unsigned rest = unsigned(w) / unsigned(n_col_tiles);
     const int kvh = int(rest % unsigned(Hkv));
     const int r = int(rest / unsigned(Hkv));
-    const int q0 = cu_q[r];
-    const int q_len = cu_q[r + 1] - q0;
+    // This item's lengths and the block ids of its first three tiles are
+    // loaded together: one round trip for all.  A block id is loaded
+    // unconditionally (clamped into the table row) and checked where it is
+    // used, so that no wait follows the scalar load.
+    const int32_t* bt = block_tables + size_t(r) * max_blocks;
+    auto raw_id = [&](int tl) { return bt[min(tl * kTileBlocks + my_blk, max_blocks - 1)]; };
+    const int q0 = cu_q[r], q_end = cu_q[r + 1], L_in = seq_lens[r];
+    const int raw_id0 = raw_id(0), raw_id1 = raw_id(1);
+    int raw_next = raw_id(2);  // raw id of the next tile to issue after tile 1
+    // First use of all six values at once: the loads are issued together and
+    // waited for once.
+    asm volatile("" : : "s"(q0), "s"(q_end), "s"(L_in), "s"(raw_id0), "s"(raw_id1), "s"(raw_next));
+    const int q_len = q_end - q0;
     const int n_cols = q_len * G;
     const int col0 = tile * kCols;
-    int L = seq_lens[r];
-    if (L > max_blocks * kBlock) L = max_blocks * kBlock;
+    const int L = min(L_in, max_blocks * kBlock);
     if (q_len <= 0 || col0 >= n_cols || q_len > L) {  // nothing to do for this item
       if (tid == 0) {
         s_item[(it + 1) & 1] = fetch();
@@ -312,6 +322,9 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const int wave_first = col0 + wave * kColsPerWave;
     const bool wave_active = wave_first < n_cols;
     const int wave_pos_min = qstart + min(wave_first, n_cols - 1) / G;
+    // Last tile holding a key some column of this wave sees (-1: no column).
+    const int wave_last =
+        wave_active ? (qstart + min(wave_first + kColsPerWave - 1, n_cols - 1) / G) / kKeys : -1;
     const int wg_pos_max = qstart + min(col0 + kCols - 1, n_cols - 1) / G;
     const int n_tiles = wg_pos_max / kKeys + 1;
     const int n_blk_used = (wg_pos_max >> 4) + 1;  // <= ceil(L / 16) <= max_blocks
@@ -321,22 +334,17 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
 #pragma unroll
     for (int kc = 0; kc < kDch; ++kc) qf[kc] = as_bf16x8(*(const u32x4*)(q + qrow + kc * 16 + hh * 8));
 
-    const int32_t* bt = block_tables + size_t(r) * max_blocks;
     const uint8_t* kbase = reinterpret_cast<const uint8_t*>(k_pool) + size_t(kvh) * kSlabBytes;
     const uint8_t* vbase = reinterpret_cast<const uint8_t*>(v_pool) + size_t(kvh) * kSlabBytes;
-    // Pool block of this wave in tile tl; unusable ids read block 0 instead
-    // (stray K rows only meet masked scores, stray V rows past key_lim are
-    // zeroed below).  A wave-uniform index: a scalar load.
-    auto block_id = [&](int tl) -> int {
-      const int i = tl * kTileBlocks + my_blk;
-      int id = i < n_blk_used ? bt[i] : 0;
-      return (id < 0 || id >= num_blocks) ? 0 : id;
+    // Pool block of this wave in tile tl, from the raw table entry; unusable
+    // ids read block 0 instead (stray K rows only meet masked scores, stray V
+    // rows past key_lim are zeroed below).
+    auto usable = [&](int tl, int id) {
+      return (tl * kTileBlocks + my_blk < n_blk_used && id >= 0 && id < num_blocks) ? id : 0;
     };
     auto stage = [&](int tl) { return ring + ((tbase + tl) % kStages) * kStageBytes; };
-    int id_next = block_id(0);
-    auto issue_tile = [&](int tl) {  // tiles are issued in order 0, 1, 2, ...
-      const int id = id_next;
-      id_next = block_id(tl + 1);
+    auto issue_tile = [&](int tl, int raw) {
+      const int id = usable(tl, raw);
       uint8_t* st = stage(tl);
       const uint8_t* ksrc = kbase + size_t(id) * slab_stride;
       const uint8_t* vsrc = vbase + size_t(id) * slab_stride;
@@ -502,11 +510,17 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
         zero_v_tail(j * kKeys, stage(j) + kKTileBytes);
         wait_lgkmcnt0();  // zeros in LDS before the next barrier
       }
-      if (j + 2 < n_tiles) issue_tile(j + 2);
+      if (j + 2 < n_tiles) issue_tile(j + 2, raw_next);
+    };
+    // The block id for begin_m(j + 1) is loaded at the start of V_j: no LDS
+    // read follows until the next phase, so the scalar load (which shares
+    // lgkmcnt with LDS reads) has landed before anything waits on lgkmcnt.
+    auto prefetch_id = [&](int j) {
+      if (j + 3 < n_tiles) raw_next = raw_id(j + 3);
     };
 
-    issue_tile(0);
-    if (1 < n_tiles) issue_tile(1);
+    issue_tile(0, raw_id0);
+    if (1 < n_tiles) issue_tile(1, raw_id1);
     if (tid == 0) {  // the next item, fetched while the first tiles load
       s_item[(it + 1) & 1] = fetch();
       wait_lgkmcnt0();
@@ -516,19 +530,23 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     wait_vmcnt<0>();
     if (lag) bare_barrier();
     begin_m(0);
-    if (wave_active) m_phase(no(), yes(), nullptr, stage(0));
+    if (0 <= wave_last) m_phase(no(), yes(), stage(0), stage(0));
     if (n_tiles > 1) wait_tile(1);
     bare_barrier();
-    if (wave_active) softmax(0);
+    prefetch_id(0);
+    if (0 <= wave_last) softmax(0);
     for (int j = 1; j < n_tiles; ++j) {
       begin_m(j);
-      if (wave_active) m_phase(yes(), yes(), stage(j - 1) + kKTileBytes, stage(j));
+      // Tiles past the wave's last visible key are skipped; the step right
+      // after it still adds P(j-1) (its S(j) product is wasted and ignored).
+      if (j - 1 <= wave_last) m_phase(yes(), yes(), stage(j - 1) + kKTileBytes, stage(j));
       if (j + 1 < n_tiles) wait_tile(j + 1);
       bare_barrier();
-      if (wave_active) softmax(j * kKeys);
+      prefetch_id(j);
+      if (j <= wave_last) softmax(j * kKeys);
     }
     begin_m(n_tiles);
-    if (wave_active) m_phase(yes(), no(), stage(n_tiles - 1) + kKTileBytes, nullptr);
+    if (n_tiles - 1 <= wave_last) m_phase(yes(), no(), stage(n_tiles - 1) + kKTileBytes, stage(0));
     if (!lag) bare_barrier();
     tbase += n_tiles;
 
