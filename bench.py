@@ -18,7 +18,10 @@ dominant kernel, the prefill attention launch, timed with HIP events on the
 stream it runs on.  ``cpu_baseline`` times the fp64 oracle on a bounded
 sample of the same workload on the host cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--cascade]
+
+``--cascade`` runs the prefill attention split at the prefix every prompt of
+the batch shares (ilpc_paged_prefill_attn_cascade).
 """
 from __future__ import annotations
 
@@ -127,6 +130,8 @@ def main():
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle attention to time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cascade", action="store_true",
+                    help="split the prefill attention at the prefix every prompt shares")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -138,7 +143,8 @@ def main():
     import torch
 
     from paper_2507_08523_amd import ilpc, workload
-    from paper_2507_08523_amd.pipeline import PagedPrefixCache, max_blocks_of, pool_blocks_needed
+    from paper_2507_08523_amd.pipeline import (PagedPrefixCache, max_blocks_of, pool_blocks_needed,
+                                               shared_prefix_len)
 
     ilpc.load()
     dev = torch.device("cuda:0")
@@ -180,6 +186,15 @@ def main():
     rows = wl.packed_suffix(cached)
     q, k_new, v_new = rows["q"], rows["k_new"], rows["v_new"]
     out = torch.empty_like(q)
+    shared_len, cascade_ws = 0, None
+    if args.cascade:
+        shared_len = shared_prefix_len(cached, tables)
+        n_ws = ilpc.attn_cascade_workspace_bytes(len(wl.prompts), int((wl.seq_lens - cached).max()),
+                                                 sp.n_q_heads, sp.n_kv_heads, sp.head_dim)
+        cascade_ws = torch.zeros(n_ws, dtype=torch.uint8, device=dev)
+        decode_ws = torch.zeros(ilpc.attn_cascade_workspace_bytes(len(wl.prompts), 1, sp.n_q_heads,
+                                                                  sp.n_kv_heads, sp.head_dim),
+                                dtype=torch.uint8, device=dev)
     L = wl.seq_lens.astype(np.int32)
     dec_in = [wl.decode_inputs(s) for s in range(dec)]
     dec_out = [torch.empty_like(d["q"]) for d in dec_in]
@@ -202,12 +217,18 @@ def main():
         e[0].record(stream)
         pc.append(b, k_new, v_new, stream)
         e[1].record(stream)
-        pc.attend(b, q, out, sp.scale, stream)
+        if args.cascade:
+            pc.attend_cascade(b, q, out, sp.scale, shared_len, cascade_ws, stream)
+        else:
+            pc.attend(b, q, out, sp.scale, stream)
         e[2].record(stream)
         for s in range(dec):
             bd = pc.upload(t, cu_dec, L + s + 1, L + s, stream)
             pc.append(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], stream)
-            pc.attend(bd, dec_in[s]["q"], dec_out[s], sp.scale, stream)
+            if args.cascade:
+                pc.attend_cascade(bd, dec_in[s]["q"], dec_out[s], sp.scale, shared_len, decode_ws, stream)
+            else:
+                pc.attend(bd, dec_in[s]["q"], dec_out[s], sp.scale, stream)
         e[3].record(stream)
         return c
 
@@ -256,7 +277,8 @@ def main():
         "config": {"workload": sp.name, "prompts": len(wl.prompts), "q_heads": sp.n_q_heads,
                    "kv_heads": sp.n_kv_heads, "head_dim": sp.head_dim, "block": 16,
                    "query_tokens": work["query_tokens"], "decode_steps": dec,
-                   "cached_fraction": round(float(cached.sum() / wl.seq_lens.sum()), 4)},
+                   "cached_fraction": round(float(cached.sum() / wl.seq_lens.sum()), 4),
+                   **({"cascade_shared_len": shared_len} if args.cascade else {})},
         "roofline": roof,
         "attn": {"launch_us": round(attn_ms * 1e3, 2), "tflops": round(tflops, 2),
                  "logical_gbs": round(gbs, 1), "flops": work["flops"], "logical_bytes": work["logical_bytes"],

@@ -191,6 +191,43 @@ int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool, const uin
                             int32_t block_size, float softmax_scale, uint16_t* out,
                             void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of device workspace ilpc_paged_prefill_attn_cascade needs:
+ * 256 + align256(B*max_q_len*Hq*D*4) + align256(B*max_q_len*Hq*8). */
+int ilpc_attn_cascade_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                                      size_t* bytes);
+
+/*
+ * The same attention as ilpc_paged_prefill_attn, split at a prefix that every
+ * request of the batch shares (the instruction and leading demonstrations of
+ * the log-parsing prompts, section 2.1.1, which prefix caching stores once,
+ * section 2.1.2): first every query row of the batch attends to the shared
+ * keys 0 .. shared_len-1 in one pass (their K/V is read once per 256 query
+ * columns of the whole batch, not once per request), then each request's
+ * queries attend to their own keys shared_len .. L_r-1 starting from that
+ * state, and the two halves are merged exactly (online-softmax rescaling).
+ *
+ * shared_len  [host] a multiple of 16 in [0, 16*max_blocks].  The caller
+ *             guarantees that the first shared_len/16 entries of every
+ *             request's block table equal request 0's, and that shared_len <=
+ *             L_r - q_len_r for every request (the shared keys precede every
+ *             query).  0 runs ilpc_paged_prefill_attn's single pass.
+ * workspace   [device] >= ilpc_attn_cascade_workspace_bytes() bytes,
+ *             16-byte aligned, its first 128 bytes zero-filled before the
+ *             first use (each call leaves them zero-filled again); the rest
+ *             holds fp32 partial results, overwritten by every call.
+ * Other arguments and the result as for ilpc_paged_prefill_attn; rows of
+ * requests whose q_len exceeds max_q_len are not computed.  If the
+ * shared_len contract does not hold the output is unspecified, but no
+ * out-of-bounds access is made.  Results agree with the single pass within
+ * rounding (the summation order differs).
+ */
+int ilpc_paged_prefill_attn_cascade(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                                    int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                                    const int32_t* cu_q, const int32_t* seq_lens, int32_t B,
+                                    int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                                    int32_t block_size, int32_t shared_len, float softmax_scale,
+                                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -39,6 +39,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;                    // tokens per pool block
 constexpr int kWaves = 8;                     // waves per attention workgroup
@@ -202,13 +203,28 @@ __device__ __forceinline__ unsigned xcd_id() {
   return static_cast<unsigned>(__builtin_amdgcn_s_getreg((31 << 11) | 20)) & 7u;
 }
 
-template <int D>
+// What one launch of the attention kernel computes.
+//   kFull:   each request's queries over all of its keys (causal).
+//   kShared: first half of a split over a prefix of kv_split keys that every
+//            request shares (same blocks, all before any query): every query
+//            row of the batch over keys [0, kv_split) of request 0's table, no
+//            mask; the unnormalised O, the running max and the sum go to
+//            part_o / part_ml instead of out.
+//   kSuffix: second half: each request's queries over keys [kv_split, L)
+//            (causal), starting from the state kShared left, normalised into out.
+// Splitting this way reads the shared K/V once per column tile of the whole
+// batch instead of once per request (the log-sum-exp merge of the two halves
+// is exact up to rounding).
+enum AttnMode { kFull = 0, kShared = 1, kSuffix = 2 };
+
+template <int D, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
     const uint16_t* __restrict__ v_pool, int num_blocks, const int32_t* __restrict__ block_tables,
-    int max_blocks, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int Hq,
-    int Hkv, int n_col_tiles, unsigned n_items, float scale_log2, uint16_t* __restrict__ out,
-    unsigned* __restrict__ queue) {
+    int max_blocks, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int n_req,
+    int Hq, int Hkv, int n_col_tiles, unsigned n_items, float scale_log2, uint16_t* __restrict__ out,
+    unsigned* __restrict__ queue, int kv_split, float* __restrict__ part_o, float* __restrict__ part_ml,
+    int part_rows) {
   constexpr int kDch = D / 16;                    // 16-wide contraction chunks of Q.K^T
   constexpr int kDt = D / 32;                     // 32-row output tiles of O^T
   constexpr int kRowBytes = D * 2;                // one K row in LDS
@@ -284,23 +300,30 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const int tile = n_col_tiles - 1 - int(unsigned(w) % unsigned(n_col_tiles));
     const unsigned rest = unsigned(w) / unsigned(n_col_tiles);
     const int kvh = int(rest % unsigned(Hkv));
-    const int r = int(rest / unsigned(Hkv));
+    const int r = MODE == kShared ? 0 : int(rest / unsigned(Hkv));
+    // First key tile of this launch (the suffix half starts at kv_split).
+    const int t0 = MODE == kSuffix ? kv_split / kKeys : 0;
     // This item's lengths and the block ids of its first three tiles are
     // loaded together: one round trip for all.  A block id is loaded
     // unconditionally (clamped into the table row) and checked where it is
     // used, so that no wait follows the scalar load.
     const int32_t* bt = block_tables + size_t(r) * max_blocks;
-    auto raw_id = [&](int tl) { return bt[min(tl * kTileBlocks + my_blk, max_blocks - 1)]; };
-    const int q0 = cu_q[r], q_end = cu_q[r + 1], L_in = seq_lens[r];
+    auto raw_id = [&](int tl) { return bt[min((t0 + tl) * kTileBlocks + my_blk, max_blocks - 1)]; };
+    // The shared half treats the whole batch as one request whose queries all
+    // follow the kv_split shared keys.
+    const int q0 = MODE == kShared ? 0 : cu_q[r];
+    const int q_end = MODE == kShared ? cu_q[n_req] : cu_q[r + 1];
+    const int L_in = MODE == kShared ? kv_split + (q_end - q0) : seq_lens[r];
     const int raw_id0 = raw_id(0), raw_id1 = raw_id(1);
     int raw_next = raw_id(2);  // raw id of the next tile to issue after tile 1
     // First use of all six values at once: the loads are issued together and
     // waited for once.
     asm volatile("" : : "s"(q0), "s"(q_end), "s"(L_in), "s"(raw_id0), "s"(raw_id1), "s"(raw_next));
-    const int q_len = q_end - q0;
+    // In the split modes, rows past the partial-state buffer are not computed.
+    const int q_len = MODE == kFull ? q_end - q0 : min(q_end, part_rows) - q0;
     const int n_cols = q_len * G;
     const int col0 = tile * kCols;
-    const int L = min(L_in, max_blocks * kBlock);
+    const int L = MODE == kShared ? L_in : min(L_in, max_blocks * kBlock);
     if (q_len <= 0 || col0 >= n_cols || q_len > L) {  // nothing to do for this item
       if (tid == 0) {
         s_item[(it + 1) & 1] = fetch();
@@ -322,13 +345,17 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const int wave_first = col0 + wave * kColsPerWave;
     const bool wave_active = wave_first < n_cols;
     const int wave_pos_min = qstart + min(wave_first, n_cols - 1) / G;
-    // Last tile holding a key some column of this wave sees (-1: no column).
-    const int wave_last =
-        wave_active ? (qstart + min(wave_first + kColsPerWave - 1, n_cols - 1) / G) / kKeys : -1;
     const int wg_pos_max = qstart + min(col0 + kCols - 1, n_cols - 1) / G;
-    const int n_tiles = wg_pos_max / kKeys + 1;
-    const int n_blk_used = (wg_pos_max >> 4) + 1;  // <= ceil(L / 16) <= max_blocks
-    const int key_lim = wg_pos_max + 1;            // keys at or past this are masked everywhere
+    // Keys at or past key_lim are masked everywhere (and their V rows zeroed).
+    const int key_lim = MODE == kShared ? kv_split : wg_pos_max + 1;
+    const int n_tiles = (key_lim - 1) / kKeys + 1 - t0;  // tiles of this launch, from t0
+    const int n_blk_used = (key_lim + kBlock - 1) / kBlock;  // <= ceil(L / 16) <= max_blocks
+    // Last tile (counted from t0) holding a key some column of this wave sees
+    // (-1: no column).
+    const int wave_last =
+        !wave_active ? -1
+        : MODE == kShared ? n_tiles - 1
+                          : (qstart + min(wave_first + kColsPerWave - 1, n_cols - 1) / G) / kKeys - t0;
 
     bf16x8 qf[kDch];
 #pragma unroll
@@ -340,7 +367,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     // ids read block 0 instead (stray K rows only meet masked scores, stray V
     // rows past key_lim are zeroed below).
     auto usable = [&](int tl, int id) {
-      return (tl * kTileBlocks + my_blk < n_blk_used && id >= 0 && id < num_blocks) ? id : 0;
+      return ((t0 + tl) * kTileBlocks + my_blk < n_blk_used && id >= 0 && id < num_blocks) ? id : 0;
     };
     auto stage = [&](int tl) { return ring + ((tbase + tl) % kStages) * kStageBytes; };
     auto issue_tile = [&](int tl, int raw) {
@@ -377,20 +404,56 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
       for (int i = 0; i < 16; ++i) o[dt][i] = 0.f;
     float m_used = -INFINITY;  // max (log2 units) the exponentials of this column are taken against
     float l_run = 0.f;         // this lane half's share of the column's exponential sum
+    const size_t prow = qrow / D;  // (query row, q head) of this lane's column
+    if constexpr (MODE == kSuffix) {
+      // Continue from the shared half's state (loaded with Q, waited for with
+      // the first tiles).  Lane half 0 carries the whole sum.
+      m_used = part_ml[prow * 2];
+      l_run = hh == 0 ? part_ml[prow * 2 + 1] : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const f32x4 v = *(const f32x4*)(part_o + prow * D + dt * 32 + g4 * 8 + hh * 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[dt][g4 * 4 + e] = v[e];
+        }
+    }
     bf16x8 pb[kTileBlocks];    // P of the tile whose V^T P^T is still due
     f32x16 sc0, sc1;           // scores of the tile whose softmax is next
 
     // Softmax step of the score tile starting at key j0: causal mask, column
     // max, lazy rescale of O, P = exp2(S * scale_log2 - m) as bf16 (the sum
     // uses the same bf16 values).
+    // Lane half hh holds keys j0 + (e>>3)*16 + 8*hh + (e&7) [+32] of the tile.
     auto softmax = [&](int j0) {
-      if (j0 + kKeys - 1 > wave_pos_min) {
+      if (MODE != kShared && j0 + kKeys - 1 > wave_pos_min) {  // causal
         const int rel = pos - j0 - hh * 8;  // key (e>>3)*16 + (e&7) [+32] is visible iff <= rel
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int k = (e >> 3) * 16 + (e & 7);
           sc0[e] = k > rel ? -INFINITY : sc0[e];
           sc1[e] = k + 32 > rel ? -INFINITY : sc1[e];
+        }
+      }
+      if (MODE == kShared && j0 + kKeys > key_lim) {  // keys past the shared prefix
+        int lim = key_lim - j0 - hh * 8;
+        asm volatile("" : "+v"(lim));  // computed here: hoisted, the 32 compares would pin 64 SGPRs
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int k = (e >> 3) * 16 + (e & 7);
+          sc0[e] = k >= lim ? -INFINITY : sc0[e];
+          sc1[e] = k + 32 >= lim ? -INFINITY : sc1[e];
+        }
+      }
+      if (MODE == kSuffix && j0 < kv_split) {  // keys of the shared prefix: done before
+        int lo = kv_split - j0 - hh * 8;
+        asm volatile("" : "+v"(lo));  // as above
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int k = (e >> 3) * 16 + (e & 7);
+          sc0[e] = k < lo ? -INFINITY : sc0[e];
+          sc1[e] = k + 32 < lo ? -INFINITY : sc1[e];
         }
       }
       float mx = max3f(sc0[0], sc1[0], sc0[1]);
@@ -506,8 +569,8 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     };
     auto begin_m = [&](int j) {
       bare_barrier();
-      if (j < n_tiles && j * kKeys + kKeys > key_lim) {
-        zero_v_tail(j * kKeys, stage(j) + kKTileBytes);
+      if (j < n_tiles && (t0 + j) * kKeys + kKeys > key_lim) {
+        zero_v_tail((t0 + j) * kKeys, stage(j) + kKTileBytes);
         wait_lgkmcnt0();  // zeros in LDS before the next barrier
       }
       if (j + 2 < n_tiles) issue_tile(j + 2, raw_next);
@@ -534,7 +597,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     if (n_tiles > 1) wait_tile(1);
     bare_barrier();
     prefetch_id(0);
-    if (0 <= wave_last) softmax(0);
+    if (0 <= wave_last) softmax(t0 * kKeys);
     for (int j = 1; j < n_tiles; ++j) {
       begin_m(j);
       // Tiles past the wave's last visible key are skipped; the step right
@@ -543,7 +606,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
       if (j + 1 < n_tiles) wait_tile(j + 1);
       bare_barrier();
       prefetch_id(j);
-      if (j <= wave_last) softmax(j * kKeys);
+      if (j <= wave_last) softmax((t0 + j) * kKeys);
     }
     begin_m(n_tiles);
     if (n_tiles - 1 <= wave_last) m_phase(yes(), no(), stage(n_tiles - 1) + kKTileBytes, stage(0));
@@ -552,18 +615,34 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
 
     if (wave_active) {
       const float l_tot = l_run + __shfl_xor(l_run, 32);
-      const float inv = 1.f / l_tot;
-      if (col_valid) {
-        uint16_t* orow = out + qrow;
-#pragma unroll
-        for (int dt = 0; dt < kDt; ++dt)
-#pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4) {
-            bf16x4 v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = (__bf16)(o[dt][g4 * 4 + e] * inv);
-            *(bf16x4*)(orow + dt * 32 + g4 * 8 + hh * 4) = v;
+      if constexpr (MODE == kShared) {  // unnormalised O, max and sum for the suffix half
+        if (col_valid) {
+          if (hh == 0) {
+            part_ml[prow * 2] = m_used;
+            part_ml[prow * 2 + 1] = l_tot;
           }
+#pragma unroll
+          for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+              const f32x4 v = {o[dt][g4 * 4], o[dt][g4 * 4 + 1], o[dt][g4 * 4 + 2], o[dt][g4 * 4 + 3]};
+              *(f32x4*)(part_o + prow * D + dt * 32 + g4 * 8 + hh * 4) = v;
+            }
+        }
+      } else {
+        const float inv = 1.f / l_tot;
+        if (col_valid) {
+          uint16_t* orow = out + qrow;
+#pragma unroll
+          for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+              bf16x4 v;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = (__bf16)(o[dt][g4 * 4 + e] * inv);
+              *(bf16x4*)(orow + dt * 32 + g4 * 8 + hh * 4) = v;
+            }
+        }
       }
     }
   }
@@ -640,6 +719,69 @@ extern "C" int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t H
   return ILPC_OK;
 }
 
+namespace {
+
+// Cascade workspace: two queue-counter blocks (one per launch), then the
+// partial O [rows, Hq, D] and (max, sum) [rows, Hq, 2] in fp32, where
+// rows = B * max_q_len; sections start on 256-byte boundaries.
+constexpr size_t kCascadeHead = 256;
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+size_t cascade_part_o_bytes(int64_t rows, int Hq, int D) { return align256(size_t(rows) * Hq * D * 4); }
+size_t cascade_bytes(int64_t rows, int Hq, int D) {
+  return kCascadeHead + cascade_part_o_bytes(rows, Hq, D) + align256(size_t(rows) * Hq * 2 * 4);
+}
+
+// Argument checks shared by both attention entry points.
+int check_attn_args(const char* fn, const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                    int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                    const int32_t* cu_q, const int32_t* seq_lens, int32_t B, int32_t max_q_len,
+                    int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size, float softmax_scale,
+                    const uint16_t* out) {
+  using ilpc::set_error;
+  if (B < 0 || max_q_len < 0 || num_blocks < 1 || max_blocks < 1 || Hq < 1 || Hkv < 1)
+    return set_error(ILPC_EINVAL, "%s: negative or zero size", fn);
+  if (block_size != kBlock) return set_error(ILPC_EUNSUP, "%s: block_size must be 16", fn);
+  if (D != 64 && D != 128) return set_error(ILPC_EUNSUP, "%s: head_dim %d unsupported", fn, D);
+  if (Hq % Hkv != 0 || Hq / Hkv > kMaxGroup)
+    return set_error(ILPC_EUNSUP, "%s: Hq %d / Hkv %d unsupported", fn, Hq, Hkv);
+  if (!std::isfinite(softmax_scale)) return set_error(ILPC_EINVAL, "%s: softmax_scale is not finite", fn);
+  if (max_blocks > kMaxTableBlocks)
+    return set_error(ILPC_EUNSUP, "%s: max_blocks %d > %d", fn, max_blocks, kMaxTableBlocks);
+  if (B == 0 || max_q_len == 0) return ILPC_OK;
+  if (!q || !k_pool || !v_pool || !block_tables || !cu_q || !seq_lens || !out)
+    return set_error(ILPC_EINVAL, "%s: NULL pointer", fn);
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
+    return set_error(ILPC_EINVAL, "%s: Q/K/V/out must be 16-byte aligned", fn);
+  if (int64_t(B) * max_q_len * (Hq / Hkv) / kCols + 1 > (int64_t(1) << 31) / Hkv)
+    return set_error(ILPC_EUNSUP, "%s: grid too large", fn);
+  return ILPC_OK;
+}
+
+// One persistent launch of mode MODE over `items` work items.
+template <int MODE>
+int launch_attn(const char* fn, const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks, const int32_t* cu_q,
+                const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int64_t col_tiles,
+                float scale_log2, uint16_t* out, unsigned* queue, int kv_split, float* part_o,
+                float* part_ml, int part_rows, hipStream_t s) {
+  const int64_t items = col_tiles * Hkv * (MODE == kShared ? 1 : B);
+  if (items == 0) return ILPC_OK;
+  const int cus = device_cus();
+  if (cus <= 0) return ilpc::set_error(ILPC_EHIP, "%s: cannot query the device", fn);
+  const unsigned grid = unsigned(items < cus ? items : cus);
+  if (D == 128)
+    hipLaunchKernelGGL((paged_attn_kernel<128, MODE>), dim3(grid), dim3(kThreads), 0, s, q, k_pool, v_pool,
+                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, B, Hq, Hkv, int(col_tiles),
+                       unsigned(items), scale_log2, out, queue, kv_split, part_o, part_ml, part_rows);
+  else
+    hipLaunchKernelGGL((paged_attn_kernel<64, MODE>), dim3(grid), dim3(kThreads), 0, s, q, k_pool, v_pool,
+                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, B, Hq, Hkv, int(col_tiles),
+                       unsigned(items), scale_log2, out, queue, kv_split, part_o, part_ml, part_rows);
+  return launch_status(fn);
+}
+
+}  // namespace
+
 extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool,
                                        const uint16_t* v_pool, int32_t num_blocks,
                                        const int32_t* block_tables, int32_t max_blocks,
@@ -647,44 +789,65 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
                                        int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
                                        int32_t block_size, float softmax_scale, uint16_t* out,
                                        void* workspace, size_t workspace_bytes, void* stream) {
-  using ilpc::set_error;
-  if (B < 0 || max_q_len < 0 || num_blocks < 1 || max_blocks < 1 || Hq < 1 || Hkv < 1)
-    return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: negative or zero size");
-  if (block_size != kBlock)
-    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: block_size must be 16");
-  if (D != 64 && D != 128)
-    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: head_dim %d unsupported", D);
-  if (Hq % Hkv != 0 || Hq / Hkv > kMaxGroup)
-    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: Hq %d / Hkv %d unsupported", Hq, Hkv);
-  if (!std::isfinite(softmax_scale))
-    return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: softmax_scale is not finite");
-  if (max_blocks > kMaxTableBlocks)
-    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: max_blocks %d > %d", max_blocks, kMaxTableBlocks);
-  if (B == 0 || max_q_len == 0) return ILPC_OK;
-  if (!q || !k_pool || !v_pool || !block_tables || !cu_q || !seq_lens || !out)
-    return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: NULL pointer");
-  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
-    return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: Q/K/V/out must be 16-byte aligned");
+  static const char* fn = "ilpc_paged_prefill_attn";
+  int rc = check_attn_args(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                           max_q_len, Hq, Hkv, D, block_size, softmax_scale, out);
+  if (rc != ILPC_OK || B == 0 || max_q_len == 0) return rc;
   if (!workspace || workspace_bytes < kQueueWords * sizeof(unsigned) || !aligned16(workspace))
-    return set_error(ILPC_EINVAL, "ilpc_paged_prefill_attn: workspace must be %zu bytes, 16-byte aligned",
-                     kQueueWords * sizeof(unsigned));
+    return ilpc::set_error(ILPC_EINVAL, "%s: workspace must be %zu bytes, 16-byte aligned", fn,
+                           kQueueWords * sizeof(unsigned));
   const int64_t col_tiles = (int64_t(max_q_len) * (Hq / Hkv) + kCols - 1) / kCols;
-  const int64_t items = col_tiles * Hkv * B;
-  if (items > (int64_t(1) << 31) - 1)
-    return set_error(ILPC_EUNSUP, "ilpc_paged_prefill_attn: grid too large");
+  return launch_attn<kFull>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                            Hq, Hkv, D, col_tiles, softmax_scale * 1.4426950408889634f, out,
+                            static_cast<unsigned*>(workspace), 0, nullptr, nullptr, 0,
+                            static_cast<hipStream_t>(stream));
+}
+
+extern "C" int ilpc_attn_cascade_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv,
+                                                 int32_t D, size_t* bytes) {
+  if (!bytes || B < 0 || max_q_len < 0 || Hq < 1 || Hkv < 1 || D < 1)
+    return ilpc::set_error(ILPC_EINVAL, "ilpc_attn_cascade_workspace_bytes: bad argument");
+  *bytes = cascade_bytes(int64_t(B) * max_q_len, Hq, D);
+  return ILPC_OK;
+}
+
+extern "C" int ilpc_paged_prefill_attn_cascade(
+    const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool, int32_t num_blocks,
+    const int32_t* block_tables, int32_t max_blocks, const int32_t* cu_q, const int32_t* seq_lens,
+    int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size,
+    int32_t shared_len, float softmax_scale, uint16_t* out, void* workspace, size_t workspace_bytes,
+    void* stream) {
+  static const char* fn = "ilpc_paged_prefill_attn_cascade";
+  int rc = check_attn_args(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                           max_q_len, Hq, Hkv, D, block_size, softmax_scale, out);
+  if (rc != ILPC_OK) return rc;
+  if (shared_len < 0 || shared_len % kBlock != 0 || shared_len > max_blocks * kBlock)
+    return ilpc::set_error(ILPC_EINVAL, "%s: shared_len %d must be a multiple of 16 in [0, 16 * max_blocks]",
+                           fn, shared_len);
+  if (B == 0 || max_q_len == 0) return ILPC_OK;
+  const int64_t rows = int64_t(B) * max_q_len;
+  if (rows * Hq > (int64_t(1) << 31) - 1) return ilpc::set_error(ILPC_EUNSUP, "%s: batch too large", fn);
+  const size_t need = cascade_bytes(rows, Hq, D);
+  if (!workspace || workspace_bytes < need || !aligned16(workspace))
+    return ilpc::set_error(ILPC_EINVAL, "%s: workspace must be %zu bytes, 16-byte aligned", fn, need);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  unsigned* queue_shared = reinterpret_cast<unsigned*>(ws);
+  unsigned* queue_suffix = reinterpret_cast<unsigned*>(ws + kQueueWords * sizeof(unsigned));
+  float* part_o = reinterpret_cast<float*>(ws + kCascadeHead);
+  float* part_ml = reinterpret_cast<float*>(ws + kCascadeHead + cascade_part_o_bytes(rows, Hq, D));
   const float scale_log2 = softmax_scale * 1.4426950408889634f;
-  const int cus = device_cus();
-  if (cus <= 0) return set_error(ILPC_EHIP, "ilpc_paged_prefill_attn: cannot query the device");
-  const unsigned grid = unsigned(items < cus ? items : cus);
-  unsigned* queue = static_cast<unsigned*>(workspace);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (D == 128)
-    hipLaunchKernelGGL(paged_attn_kernel<128>, dim3(grid), dim3(kThreads), 0, s, q, k_pool, v_pool,
-                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv, int(col_tiles),
-                       unsigned(items), scale_log2, out, queue);
-  else
-    hipLaunchKernelGGL(paged_attn_kernel<64>, dim3(grid), dim3(kThreads), 0, s, q, k_pool, v_pool,
-                       num_blocks, block_tables, max_blocks, cu_q, seq_lens, Hq, Hkv, int(col_tiles),
-                       unsigned(items), scale_log2, out, queue);
-  return launch_status("ilpc_paged_prefill_attn");
+  const int G = Hq / Hkv;
+  const int64_t col_tiles = (int64_t(max_q_len) * G + kCols - 1) / kCols;
+  if (shared_len == 0)
+    return launch_attn<kFull>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens,
+                              B, Hq, Hkv, D, col_tiles, scale_log2, out, queue_shared, 0, nullptr, nullptr,
+                              0, s);
+  rc = launch_attn<kShared>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                            Hq, Hkv, D, (rows * G + kCols - 1) / kCols, scale_log2, out, queue_shared,
+                            shared_len, part_o, part_ml, int(rows), s);
+  if (rc != ILPC_OK) return rc;
+  return launch_attn<kSuffix>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                              Hq, Hkv, D, col_tiles, scale_log2, out, queue_suffix, shared_len, part_o,
+                              part_ml, int(rows), s);
 }

@@ -108,6 +108,37 @@ class PagedPrefixCache:
         ilpc.paged_prefill_attn(q, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
                                 batch.seq_lens, batch.max_q_len, scale, out, None, stream)
 
+    def attend_cascade(self, batch: DeviceBatch, q, out, scale: float, shared_len: int, workspace,
+                       stream=None):
+        """Attention split at `shared_len` keys every request shares (see shared_prefix_len)."""
+        ilpc.paged_prefill_attn_cascade(q, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
+                                        batch.seq_lens, batch.max_q_len, shared_len, scale, out,
+                                        workspace, stream)
+
+    def cascade_workspace(self, batch: DeviceBatch, n_q_heads: int):
+        """A workspace for attend_cascade on this batch shape (first 128 bytes zeroed)."""
+        import torch
+
+        n = ilpc.attn_cascade_workspace_bytes(batch.B, batch.max_q_len, n_q_heads, self.n_kv_heads,
+                                              self.head_dim)
+        ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+        ws[:128].zero_()
+        return ws
+
+
+def shared_prefix_len(cached_len, block_tables) -> int:
+    """Keys at the front that every request of a batch shares: the longest run of
+    leading block ids equal across all rows of the host block table, capped by
+    the shortest cached prefix (so the shared keys precede every query)."""
+    cached_len = np.asarray(cached_len)
+    t = np.asarray(block_tables)
+    if len(cached_len) == 0:
+        return 0
+    n = int(cached_len.min()) // BLOCK
+    same = (t[:, :n] == t[0, :n]).all(axis=0) & (t[0, :n] >= 0)
+    run = n if same.all() else int(np.argmin(same))
+    return run * BLOCK
+
 
 def pool_blocks_needed(wl) -> int:
     """Blocks a workload's warm + measured batches can allocate (no reuse assumed)."""

@@ -88,6 +88,10 @@ SPECS: dict[str, WorkloadSpec] = {
     "sweep50": _sweep(50, 4, "shared"),
     "sweep75": _sweep(75, 8, "shared"),
     "sweep100": _sweep(100, 12, "shared"),
+    # the same fully shared batch generating 32 output tokens per prompt (the
+    # short template each log query is parsed into)
+    "sweep100_decode": WorkloadSpec(**{**_sweep(100, 12, "shared").__dict__, "name": "sweep100_decode",
+                                       "decode_steps": 32}),
     # large context: 16 of 128 demos x 128 tokens + 64-token query, then 32 decode steps
     "large": WorkloadSpec(name="large", n_q_heads=64, n_kv_heads=8, head_dim=128, n_prompts=512,
                           instr_len=0, n_demos=16, demo_len=128, pool_size=128, query_len=(64, 64),

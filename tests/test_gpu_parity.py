@@ -311,3 +311,98 @@ def test_work_queue_workspace_reused_and_left_zeroed():
         assert torch.equal(o, outs[0])
     assert int(ws.count_nonzero()) == 0
     assert int(ilpc.attn_workspace(None, side).count_nonzero()) == 0
+
+
+# -- shared-prefix split (cascade) -------------------------------------------
+
+def _cascade(run, shared_len=None):
+    from paper_2507_08523_amd.pipeline import shared_prefix_len
+
+    sl = shared_prefix_len(run.cached, run._phys(run.tables)) if shared_len is None else shared_len
+    ws = run.pc.cascade_workspace(run.batch, run.wl.spec.n_q_heads)
+    out = torch.full_like(run.rows["q"], float("nan"))
+    run.pc.attend_cascade(run.batch, run.rows["q"], out, run.wl.spec.scale, sl, ws)
+    torch.cuda.synchronize()
+    return sl, out, ws
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "sweep100", "qwen7b"])
+def test_cascade_against_oracle(name):
+    # All query rows of the batch attend to the shared prefix in one pass, then
+    # each request to its own keys, merged by rescaling: same result as the
+    # single pass within the tolerance, and the queue counters left zeroed.
+    run = Run(name)
+    sl, out, ws = _cascade(run)
+    log(f"[cascade] {name}: shared_len={sl}")
+    assert sl > 0
+    run.out = out
+    run.check(range(len(run.wl.prompts)) if name in ("tiny", "llama8b") else _sample(run, 8), tag=" cascade")
+    assert int(ws[:128].count_nonzero()) == 0
+
+
+@pytest.mark.parametrize("shared_len", [16, 48, 112])
+def test_cascade_split_inside_a_tile(shared_len):
+    # Split points that cut a 64-key tile: the shared half masks keys past the
+    # split, the suffix half the keys before it.
+    run = Run("llama8b")
+    sl, out, _ = _cascade(run, shared_len)
+    run.out = out
+    run.check(range(0, len(run.wl.prompts), 4), tag=f" cascade@{sl}")
+
+
+def test_cascade_zero_shared_len_is_the_single_pass():
+    run = Run("llama8b")
+    _, out, _ = _cascade(run, 0)
+    assert torch.equal(out, run.attend())
+
+
+def test_cascade_abi_rejections():
+    run = Run("tiny")
+    b, pc, q = run.batch, run.pc, run.rows["q"]
+    lib = ilpc.load()
+    ws = pc.cascade_workspace(b, run.wl.spec.n_q_heads)
+
+    def call(shared_len, ws_bytes):
+        return lib.ilpc_paged_prefill_attn_cascade(
+            q.data_ptr(), pc.k_pool.data_ptr(), pc.v_pool.data_ptr(), pc.num_blocks, b.block_tables.data_ptr(),
+            pc.max_blocks, b.cu_q.data_ptr(), b.seq_lens.data_ptr(), b.B, b.max_q_len, 4, 1, 64, 16, shared_len,
+            0.125, run.out.data_ptr(), ws.data_ptr(), ws_bytes, None)
+
+    assert call(8, ws.numel()) == ilpc.EINVAL                          # not a multiple of 16
+    assert call(-16, ws.numel()) == ilpc.EINVAL
+    assert call(16 * (pc.max_blocks + 1), ws.numel()) == ilpc.EINVAL   # past the table
+    assert call(64, ws.numel() - 1) == ilpc.EINVAL                      # short workspace
+    assert call(64, ws.numel()) == ilpc.OK
+    torch.cuda.synchronize()
+
+
+def test_cascade_decode_steps_against_oracle():
+    # Decode over a prefix all prompts share: every step splits at the shared
+    # prefix (one query row per prompt, all rows in one shared pass).
+    from paper_2507_08523_amd.pipeline import shared_prefix_len
+
+    run = Run(workload.scaled_spec("sweep100_decode", 32, decode_steps=6))
+    wl, pc = run.wl, run.pc
+    B = len(wl.prompts)
+    L = wl.seq_lens.astype(np.int32)
+    cu = np.arange(B + 1, dtype=np.int32)
+    sl = shared_prefix_len(run.cached, run.tables)
+    assert sl == 976
+    ws = torch.zeros(ilpc.attn_cascade_workspace_bytes(B, 1, wl.spec.n_q_heads, wl.spec.n_kv_heads,
+                                                       wl.spec.head_dim), dtype=torch.uint8, device="cuda")
+    worst = 0.0
+    for s in range(wl.spec.decode_steps):
+        d = wl.decode_inputs(s)
+        b = pc.upload(run.tables, cu, L + s + 1, L + s)
+        pc.append(b, d["k_new"], d["v_new"])
+        out = torch.full_like(d["q"], float("nan"))
+        pc.attend_cascade(b, d["q"], out, wl.spec.scale, sl, ws)
+        torch.cuda.synchronize()
+        for r in (0, 7, B - 1):
+            k, v = wl.dense_kv(r, int(L[r]) + s + 1)
+            ref = decode_step_ref(d["q"][r].float().cpu().numpy(), k.float().cpu().numpy(),
+                                  v.float().cpu().numpy(), wl.spec.scale)
+            err = np.abs(out[r].float().cpu().numpy() - ref)
+            worst = max(worst, float(err.max()))
+            assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (s, r)
+    log(f"[parity] sweep100 decode (cascade): {wl.spec.decode_steps} steps, max_abs={worst:.3e}")

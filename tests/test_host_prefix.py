@@ -198,3 +198,24 @@ def test_attn_workspace_bytes_host_only():
     with pytest.raises(ilpc.ILPCError) as e:
         ilpc.attn_workspace_bytes(-1, 0, 1, 1, 64)
     assert e.value.code == ilpc.EINVAL
+
+
+def test_shared_prefix_len_host_helper():
+    from paper_2507_08523_amd.pipeline import shared_prefix_len
+
+    t = np.array([[5, 6, 7, 9, -1], [5, 6, 7, 10, 11], [5, 6, 8, 12, -1]], np.int32)
+    assert shared_prefix_len([64, 64, 64], t) == 32          # ids agree on blocks 0, 1
+    assert shared_prefix_len([16, 64, 64], t) == 16          # capped by the shortest cached prefix
+    assert shared_prefix_len([0, 64, 64], t) == 0
+    assert shared_prefix_len([48, 48], t[:2]) == 48
+    assert shared_prefix_len([], t[:0]) == 0
+
+
+def test_cascade_workspace_bytes_host_only():
+    # 256-byte head (two 64-byte queue blocks), then fp32 O and (max, sum) per row and head
+    rows, Hq, D = 8 * 100, 32, 128
+    o_bytes = -(-rows * Hq * D * 4 // 256) * 256
+    ml_bytes = -(-rows * Hq * 8 // 256) * 256
+    assert ilpc.attn_cascade_workspace_bytes(8, 100, Hq, 8, D) == 256 + o_bytes + ml_bytes
+    with pytest.raises(ilpc.ILPCError):
+        ilpc.attn_cascade_workspace_bytes(-1, 0, 1, 1, 64)
