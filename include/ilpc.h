@@ -228,6 +228,61 @@ int ilpc_paged_prefill_attn_cascade(const uint16_t* q, const uint16_t* k_pool, c
                                     int32_t block_size, int32_t shared_len, float softmax_scale,
                                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Prefix-aware refinement of in-context demonstrations (section 3.2.1,
+ * "Prefix-Aware ICL Refinement", with its matching / modifying / reordering
+ * figure, and section 3.2.2, "ICL Table Management").  Host only,
+ * synchronous; the table is library-owned host memory.
+ *
+ * A demonstration is a (template id, demonstration id) pair of int32 values:
+ * the template it is labelled with and the concrete log (so, its tokens).  A
+ * demonstration set (DS) is an ordered list of n_demos of them.  The ICL table
+ * keeps the sets of past requests in least-recently-used order.
+ */
+typedef struct ilpc_pair_table ilpc_pair_table; /* opaque, host memory, library-owned */
+
+/* Create an empty ICL table holding at most `capacity` sets (1 .. 2^24) of
+ * `n_demos` demonstrations (1 .. 4096).  *out receives the handle. */
+int ilpc_pair_create(int32_t capacity, int32_t n_demos, ilpc_pair_table** out);
+
+/* Free a table (NULL is ignored). */
+void ilpc_pair_destroy(ilpc_pair_table* table);
+
+/* Empty the table. */
+int ilpc_pair_reset(ilpc_pair_table* table);
+
+/*
+ * Refine B requests' demonstration sets in order, each against the table as
+ * the previous requests left it (a request's set enters the table as after
+ * its inference completed).
+ *
+ * templates, demos         [host] int32 [B*n_demos]  current sets, request-major
+ * out_templates, out_demos [host] int32 [B*n_demos]  out: final sets
+ * pmc                      [host] int32 [B]          out: prefix-matching count
+ *
+ * PMC of a past set H against the current set C: the number of leading
+ * demonstrations of H whose templates all occur in C, each demonstration of
+ * C serving at most one of them.  The target is the past set of largest PMC,
+ * ties going to the most recently used; PMC 0 means no target.  Final set:
+ * the target's first PMC demonstrations in the target's order (each replacing
+ * the first not yet replaced current demonstration of its template), then
+ * the remaining current demonstrations in their order.  Table update:
+ * PMC = n_demos reuses the target (final = target) and makes it the most
+ * recently used; PMC = 0 appends the current set unchanged; otherwise the
+ * final set is appended and the target keeps its place.  A set already held
+ * is stored once (appending it refreshes it); beyond the capacity the least
+ * recently used set is evicted.  On error the table is unchanged only if the
+ * error is reported before the first request (NULL pointer, negative B).
+ */
+int ilpc_pair_refine(ilpc_pair_table* table, const int32_t* templates, const int32_t* demos, int32_t B,
+                     int32_t* out_templates, int32_t* out_demos, int32_t* pmc);
+
+/* Copy the held sets, least recently used first, into templates / demos
+ * [host] int32 [max_entries*n_demos]; *n_entries receives their number
+ * (ILPC_EINVAL, with *n_entries set, if they do not fit). */
+int ilpc_pair_entries(const ilpc_pair_table* table, int32_t* templates, int32_t* demos, int32_t max_entries,
+                      int32_t* n_entries);
+
 #ifdef __cplusplus
 }
 #endif

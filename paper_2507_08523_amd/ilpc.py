@@ -44,6 +44,11 @@ _SIGS = [
     ("ilpc_paged_prefill_attn_cascade", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32,
                                                _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                                ctypes.c_size_t, _vp]),
+    ("ilpc_pair_create", _i32, [_i32, _i32, ctypes.POINTER(_vp)]),
+    ("ilpc_pair_destroy", None, [_vp]),
+    ("ilpc_pair_reset", _i32, [_vp]),
+    ("ilpc_pair_refine", _i32, [_vp, _vp, _vp, _i32, _vp, _vp, _vp]),
+    ("ilpc_pair_entries", _i32, [_vp, _vp, _vp, _i32, ctypes.POINTER(_i32)]),
 ]
 SYMBOLS = [s[0] for s in _SIGS]
 
@@ -90,9 +95,9 @@ class PrefixCache:
         self._h = h
 
     def close(self):
-        if getattr(self, "_h", None):
-            load().ilpc_cache_destroy(self._h)
-            self._h = None
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:  # (at interpreter exit the library may be gone already)
+            _lib.ilpc_cache_destroy(h)
 
     __del__ = close
 
@@ -138,6 +143,57 @@ class PrefixCache:
         _check(load().ilpc_prefix_match(self._h, _np_ptr(tok), _np_ptr(cu), B, _np_ptr(res), max_blocks,
                                         flags, _np_ptr(cached), _np_ptr(tables), _np_ptr(keys)))
         return cached, tables, keys
+
+
+class PairTable:
+    """ICL table of prefix-aware demonstration refinement (host, library-owned).
+
+    A demonstration is a (template id, demonstration id) pair of int32; a
+    demonstration set is ``n_demos`` of them.
+    """
+
+    def __init__(self, capacity: int, n_demos: int):
+        lib = load()
+        h = ctypes.c_void_p()
+        _check(lib.ilpc_pair_create(capacity, n_demos, ctypes.byref(h)))
+        self._h, self.capacity, self.n_demos = h, capacity, n_demos
+
+    def close(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.ilpc_pair_destroy(h)
+
+    __del__ = close
+
+    def reset(self):
+        _check(load().ilpc_pair_reset(self._h))
+
+    def refine(self, templates, demos):
+        """Refine B requests' sets in order.
+
+        templates, demos: int32 [B, n_demos].  Returns (final templates, final
+        demos) int32 [B, n_demos] and the PMC of each request int32 [B].
+        """
+        t = np.ascontiguousarray(templates, dtype=np.int32)
+        d = np.ascontiguousarray(demos, dtype=np.int32)
+        if t.ndim != 2 or t.shape != d.shape or t.shape[1] != self.n_demos:
+            raise ILPCError(EINVAL, f"refine: templates and demos must both be [B, {self.n_demos}]")
+        B = t.shape[0]
+        ot, od = np.zeros_like(t), np.zeros_like(d)
+        pmc = np.zeros(B, np.int32)
+        if B:
+            _check(load().ilpc_pair_refine(self._h, _np_ptr(t), _np_ptr(d), B, _np_ptr(ot), _np_ptr(od),
+                                           _np_ptr(pmc)))
+        return ot, od, pmc
+
+    def entries(self):
+        """Held sets, least recently used first: (templates, demos) int32 [E, n_demos]."""
+        n = ctypes.c_int32()
+        cap = self.capacity
+        t = np.zeros((cap, self.n_demos), np.int32)
+        d = np.zeros_like(t)
+        _check(load().ilpc_pair_entries(self._h, _np_ptr(t), _np_ptr(d), cap, ctypes.byref(n)))
+        return t[:n.value].copy(), d[:n.value].copy()
 
 
 # -- device steps ------------------------------------------------------------
