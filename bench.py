@@ -18,10 +18,18 @@ dominant kernel, the prefill attention launch, timed with HIP events on the
 stream it runs on.  ``cpu_baseline`` times the fp64 oracle on a bounded
 sample of the same workload on the host cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--cascade]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--cascade] [--no-pair]
 
 ``--cascade`` runs the prefill attention split at the prefix every prompt of
 the batch shares (ilpc_paged_prefill_attn_cascade).
+
+ICL stream workloads (``icl_llama8b``): 2000 log-parsing requests whose
+demonstrations a selector picks with hot templates.  Before the timed steps the
+whole stream passes the ICL table (prefix-aware refinement, host C++) in
+arrival order, 64 requests per call; the earlier requests' blocks fill the
+cache and the last 64 requests are the measured batch.  ``config`` adds the
+stream's prefix-cache hit rate with and without refinement.  ``--no-pair``
+measures the batch in the selector's order.
 """
 from __future__ import annotations
 
@@ -122,6 +130,31 @@ def cpu_baseline(wl, cached_len, budget_s: float):
                        f"{t_attn:.1f} s); host nproc={os.cpu_count()}")}
 
 
+def icl_stream_workload(name: str, pair: bool):
+    """The measured batch of an ICL request stream, demonstrations refined by
+    the ICL table (or in the selector's order), and the stream's hit rates."""
+    from paper_2507_08523_amd import workload
+    from paper_2507_08523_amd.pipeline import ICL_TABLE_CAPACITY, pair_refine_stream, stream_hit_rate
+
+    sp = workload.SPECS[name]
+    st = workload.icl_stream(sp)
+    R = len(st.templates)
+    naive = stream_hit_rate(st.prompts(), sp.n_prompts)
+    info = {"stream_requests": R, "pair": pair, "stream_hit_rate_naive": round(naive["hit_rate"], 4)}
+    demos = None
+    if pair:
+        t0 = time.perf_counter()
+        _, demos, pmc = pair_refine_stream(st, ICL_TABLE_CAPACITY, sp.n_prompts)
+        dt = time.perf_counter() - t0
+        refined = stream_hit_rate(st.prompts(demos=demos), sp.n_prompts)
+        info.update({"icl_table_capacity": ICL_TABLE_CAPACITY,
+                     "stream_hit_rate": round(refined["hit_rate"], 4),
+                     "hit_rate_gain": round(refined["hit_rate"] / naive["hit_rate"], 3),
+                     "mean_pmc": round(float(pmc.mean()), 3),
+                     "pair_us_per_request": round(dt / R * 1e6, 3)})
+    return info, workload.build(sp, demos=demos)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -130,6 +163,8 @@ def main():
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle attention to time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-pair", action="store_true",
+                    help="ICL stream workloads: serve the selector's demonstration order unrefined")
     ap.add_argument("--cascade", action="store_true",
                     help="split the prefill attention at the prefix every prompt shares")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -159,7 +194,11 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
-    wl = workload.build(args.workload)
+    icl = None
+    if workload.SPECS[args.workload].n_templates:
+        icl, wl = icl_stream_workload(args.workload, not args.no_pair)
+    else:
+        wl = workload.build(args.workload)
     wl.materialize(dev)
     sp = wl.spec
     pc = PagedPrefixCache(sp.n_kv_heads, sp.head_dim, pool_blocks_needed(wl), max_blocks_of(wl),
@@ -278,7 +317,8 @@ def main():
                    "kv_heads": sp.n_kv_heads, "head_dim": sp.head_dim, "block": 16,
                    "query_tokens": work["query_tokens"], "decode_steps": dec,
                    "cached_fraction": round(float(cached.sum() / wl.seq_lens.sum()), 4),
-                   **({"cascade_shared_len": shared_len} if args.cascade else {})},
+                   **({"cascade_shared_len": shared_len} if args.cascade else {}),
+                   **(icl or {})},
         "roofline": roof,
         "attn": {"launch_us": round(attn_ms * 1e3, 2), "tflops": round(tflops, 2),
                  "logical_gbs": round(gbs, 1), "flops": work["flops"], "logical_bytes": work["logical_bytes"],

@@ -51,6 +51,11 @@ class WorkloadSpec:
     warm: str = "shared"          # "shared" | "none" | "own_prefix"
     own_prefix_len: int = 0       # for warm == "own_prefix"
     shared_demos: int | None = None  # leading demos common to all prompts; rest private
+    # ICL stream (n_templates > 0): template-labelled candidate demonstrations,
+    # a stream of `history` requests served before the measured batch
+    n_templates: int = 0
+    logs_per_template: int = 0
+    history: int = 0
     seed: int = 0
 
     @property
@@ -101,6 +106,79 @@ SPECS: dict[str, WorkloadSpec] = {
                                      demo_len=128, pool_size=128, query_len=(64, 64),
                                      warm="own_prefix", own_prefix_len=2048, seed=400),
 }
+
+
+# Log-parsing request stream with template-labelled demonstrations, on the
+# Llama-3-8B-shaped layer: 200 candidate logs (40 templates x 5 logs), 5
+# demonstrations per request, 2000 requests (the size of one Loghub-2k dataset),
+# the last 64 of which form the measured batch.
+_ICL = dict(n_q_heads=32, n_kv_heads=8, head_dim=128, n_prompts=64, instr_len=256, n_demos=5,
+            demo_len=60, pool_size=200, query_len=(48, 48), warm="history", n_templates=40,
+            logs_per_template=5, history=1936, seed=500)
+SPECS["icl_llama8b"] = WorkloadSpec(name="icl_llama8b", **_ICL)
+
+# Weights of the template draw of an ICL stream, hottest first; every other
+# template weighs TAIL_WEIGHT.  Drawing 5 distinct templates of 40 by successive
+# weighted sampling without replacement, these put the five hottest templates
+# into 36.2%, 27.2%, 24.7%, 21.2% and 17.1% of requests, the hotspot
+# selection frequencies InferLog reports (section 2.2.2, hotspot demonstrations).
+HOT_WEIGHTS = (1.0, 0.7075, 0.6350, 0.5327, 0.4240)
+TAIL_WEIGHT = 0.2563
+
+
+@dataclass
+class IclStream:
+    """The demonstration sets a kNN selector would pick for a request stream.
+
+    templates, demos: int32 [R, n_demos] in selection order (the order the
+    selector emits, least similar first); demonstration d is candidate log d,
+    of template d // logs_per_template, with tokens demo_tokens[d].
+    """
+
+    spec: WorkloadSpec
+    instr: np.ndarray
+    demo_tokens: np.ndarray
+    templates: np.ndarray
+    demos: np.ndarray
+    queries: list
+
+    def prompts(self, templates=None, demos=None):
+        """Instruction + demonstrations (in the given order) + query, per request."""
+        d = self.demos if demos is None else np.asarray(demos)
+        return [np.concatenate([self.instr, *self.demo_tokens[d[r]], self.queries[r]]).astype(np.int32)
+                for r in range(len(self.queries))]
+
+
+def icl_stream(spec: WorkloadSpec | str) -> IclStream:
+    """Seeded stand-in for kNN demonstration selection over a request stream.
+
+    Per request: n_demos distinct templates drawn by weighted sampling without
+    replacement (hot templates per HOT_WEIGHTS), one candidate log of each drawn
+    uniformly, the set in a fresh random order (similarity to each query log
+    differs), then a query log of uniform random tokens.
+    """
+    if isinstance(spec, str):
+        spec = SPECS[spec]
+    T, m, k = spec.n_templates, spec.logs_per_template, spec.n_demos
+    if T < k or m < 1 or spec.pool_size != T * m:
+        raise ValueError("ICL stream needs n_templates >= n_demos and pool_size = n_templates * logs")
+    rng = np.random.default_rng(spec.seed)
+    instr = rng.integers(0, VOCAB, spec.instr_len, dtype=np.int64).astype(np.int32)
+    demo_tokens = rng.integers(0, VOCAB, (T * m, spec.demo_len), dtype=np.int64).astype(np.int32)
+    w = np.full(T, TAIL_WEIGHT)
+    w[:min(T, len(HOT_WEIGHTS))] = HOT_WEIGHTS[:T]
+    R = spec.history + spec.n_prompts
+    # successive sampling without replacement == top-k of log-weight + Gumbel noise
+    key = np.log(w)[None, :] + rng.gumbel(size=(R, T))
+    chosen = np.argsort(-key, axis=1, kind="stable")[:, :k]
+    order = np.argsort(rng.random((R, k)), axis=1)
+    templates = np.take_along_axis(chosen, order, axis=1).astype(np.int32)
+    demos = (templates * m + rng.integers(0, m, (R, k))).astype(np.int32)
+    lo, hi = spec.query_len
+    queries = [rng.integers(0, VOCAB, int(rng.integers(lo, hi + 1)), dtype=np.int64).astype(np.int32)
+               for _ in range(R)]
+    return IclStream(spec=spec, instr=instr, demo_tokens=demo_tokens, templates=templates, demos=demos,
+                     queries=queries)
 
 
 def scaled_spec(name: str, n_prompts: int, **over) -> WorkloadSpec:
@@ -239,10 +317,19 @@ def _randn_bf16(shape, std, gen, dev):
     return out
 
 
-def build(spec: WorkloadSpec | str) -> Workload:
-    """Token streams, warm batch and slab maps for ``spec`` (no tensors yet)."""
+def build(spec: WorkloadSpec | str, demos=None) -> Workload:
+    """Token streams, warm batch and slab maps for ``spec`` (no tensors yet).
+
+    For an ICL stream, ``demos`` (int32 [history + n_prompts, n_demos]) are the
+    demonstration ids each request finally carries, in order; by default the
+    selector's own sets and order.
+    """
     if isinstance(spec, str):
         spec = SPECS[spec]
+    if spec.n_templates:
+        st = icl_stream(spec)
+        everything = st.prompts(demos=demos)
+        return _from_prompts(spec, everything[spec.history:], everything[:spec.history])
     rng = np.random.default_rng(spec.seed)
     instr = rng.integers(0, VOCAB, spec.instr_len, dtype=np.int64).astype(np.int32)
     pool = rng.integers(0, VOCAB, (spec.pool_size, spec.demo_len), dtype=np.int64).astype(np.int32)
@@ -265,7 +352,17 @@ def build(spec: WorkloadSpec | str) -> Workload:
         q_len = int(rng.integers(lo, hi + 1))
         parts.append(rng.integers(0, VOCAB, q_len, dtype=np.int64).astype(np.int32))
         prompts.append(np.concatenate(parts).astype(np.int32))
+    return _from_prompts(spec, prompts, None)
 
+
+def _from_prompts(spec: WorkloadSpec, prompts: list, history) -> Workload:
+    """Content addressing and warm batch of a measured batch ``prompts``.
+
+    ``history`` (warm mode "history"): earlier requests whose full blocks are
+    all in the cache when the measured batch arrives; the warm batch is then,
+    per measured prompt, its longest run of leading full blocks that some
+    earlier request holds token for token.
+    """
     # content addressing: one node per distinct full-block token prefix
     node_of: dict = {}
     full_nodes = []
@@ -305,6 +402,24 @@ def build(spec: WorkloadSpec | str) -> Workload:
             if s and nodes[s - 1] not in seen:
                 seen.add(nodes[s - 1])
                 warm.append(prompts[r][: s * BLOCK].copy())
+                warm_src.append(r)
+    elif spec.warm == "history":
+        held: dict = {}   # (parent node, block tokens) -> node, over the history
+        for p in history:
+            parent = -1
+            for b in range(len(p) // BLOCK):
+                parent = held.setdefault((parent, p[b * BLOCK:(b + 1) * BLOCK].tobytes()), len(held))
+        seen = set()
+        for r, p in enumerate(prompts):
+            s, parent = 0, -1
+            while s < len(p) // BLOCK:
+                parent = held.get((parent, p[s * BLOCK:(s + 1) * BLOCK].tobytes()))
+                if parent is None:
+                    break
+                s += 1
+            if s and full_nodes[r][s - 1] not in seen:
+                seen.add(full_nodes[r][s - 1])
+                warm.append(p[: s * BLOCK].copy())
                 warm_src.append(r)
     elif spec.warm == "own_prefix":
         warm = [p[: spec.own_prefix_len].copy() for p in prompts]

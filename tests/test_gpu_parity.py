@@ -41,8 +41,8 @@ def log(*a):
 class Run:
     """Warm + measured pass of one workload through the library."""
 
-    def __init__(self, spec, flags=0, perm_seed=None, table_log2_cap=20):
-        self.wl = wl = workload.build(spec)
+    def __init__(self, spec, flags=0, perm_seed=None, table_log2_cap=20, demos=None):
+        self.wl = wl = workload.build(spec, demos=demos)
         wl.materialize("cuda")
         sp = wl.spec
         nb = pool_blocks_needed(wl)
@@ -121,6 +121,21 @@ def _sample(run, n_rand, seed=0):
 def test_prefill_full_check(name):
     run = Run(name)
     run.check(range(len(run.wl.prompts)))
+
+
+@pytest.mark.parametrize("pair", [True, False])
+def test_icl_stream_batch_full_check(pair):
+    """The measured batch of the 2000-request ICL stream, demonstrations refined
+    by the ICL table (or in the selector's order), checked in full."""
+    from paper_2507_08523_amd.pipeline import ICL_TABLE_CAPACITY, pair_refine_stream
+
+    sp = workload.SPECS["icl_llama8b"]
+    demos = None
+    if pair:
+        _, demos, _ = pair_refine_stream(workload.icl_stream(sp), ICL_TABLE_CAPACITY, sp.n_prompts)
+    run = Run(sp, demos=demos)
+    assert run.cached.min() >= sp.instr_len
+    run.check(range(len(run.wl.prompts)), tag=" pair" if pair else " naive")
 
 
 def test_qwen7b_full_size_sampled():

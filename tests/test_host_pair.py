@@ -143,3 +143,59 @@ def test_argument_errors():
     lib = ilpc.load()
     assert lib.ilpc_pair_refine(None, None, None, 1, None, None, None) != 0
     assert lib.ilpc_pair_reset(None) != 0
+
+
+# -- the ICL request stream and what refinement does to its cache hits ---------
+
+from paper_2507_08523_amd import pipeline, workload  # noqa: E402
+
+
+def test_icl_stream_hotspot_frequencies():
+    """The five hottest templates land in about 36.2/27.2/24.7/21.2/17.1% of requests."""
+    st = workload.icl_stream("icl_llama8b")
+    R, k = st.templates.shape
+    assert R == 2000 and k == 5
+    assert all(len(set(row)) == k for row in st.templates.tolist())
+    assert (st.demos // st.spec.logs_per_template == st.templates).all()
+    freq = np.sort(np.bincount(st.templates.ravel(), minlength=st.spec.n_templates) / R)[::-1][:5]
+    np.testing.assert_allclose(freq, [0.362, 0.272, 0.247, 0.212, 0.171], atol=0.03)
+
+
+def _small_icl(history=400, n_prompts=16):
+    return workload.scaled_spec("icl_llama8b", n_prompts, history=history)
+
+
+def test_history_warm_batch_gives_the_stream_cache_state():
+    """The measured batch's cached lengths after the derived warm batch equal
+    those after serving the whole history through the prefix cache."""
+    sp = _small_icl()
+    st = workload.icl_stream(sp)
+    _, fd, _ = pipeline.pair_refine_stream(st, 64, sp.n_prompts)
+    prompts = st.prompts(demos=fd)
+    hist, meas = prompts[:sp.history], prompts[sp.history:]
+    nb = sum(-(-len(p) // 16) for p in prompts) + 1
+    a = ilpc.PrefixCache(nb, 16)
+    for s in range(0, len(hist), sp.n_prompts):
+        a.match(hist[s:s + sp.n_prompts])
+    c_stream, _, _ = a.match(meas)
+    wl = workload.build(sp, demos=fd)
+    assert all(np.array_equal(x, y) for x, y in zip(wl.prompts, meas))
+    b = ilpc.PrefixCache(nb, 16)
+    b.match(wl.warm)
+    c_warm, _, _ = b.match(wl.prompts)
+    assert np.array_equal(c_stream, c_warm)
+    assert c_warm.min() >= 256  # the instruction is always held
+
+
+def test_refinement_raises_the_stream_hit_rate():
+    sp = _small_icl(history=800)
+    st = workload.icl_stream(sp)
+    naive = pipeline.stream_hit_rate(st.prompts(), sp.n_prompts)
+    ft, fd, pmc = pipeline.pair_refine_stream(st, pipeline.ICL_TABLE_CAPACITY, sp.n_prompts)
+    # refinement only reorders and swaps logs of the same template
+    assert (np.sort(ft, axis=1) == np.sort(st.templates, axis=1)).all()
+    assert (fd // sp.logs_per_template == ft).all()
+    pair = pipeline.stream_hit_rate(st.prompts(demos=fd), sp.n_prompts)
+    assert pair["prompt_tokens"] == naive["prompt_tokens"]
+    assert pair["hit_rate"] > 1.1 * naive["hit_rate"], (naive, pair)
+    assert pmc.max() == sp.n_demos and pmc.min() == 0
