@@ -15,6 +15,10 @@ InferLog paper (arXiv 2507.08523) it follows.
 * ``attn_ref``    -- dense float64 causal grouped-query attention of the
   uncached suffix over cached + new keys (paper section 2.1.2: prefill over the
   prompt, KV of cache-missing tokens computed and stored, section 3.2.2).
+* ``pair_ref``    -- prefix-aware refinement of the in-context demonstrations
+  and the ICL table (sections 3.2.1 and 3.2.2).
+* ``lifecycle_ref`` -- the prefix cache with reference-counted blocks and
+  least-recently-used eviction (section 2.1.2).
 
 Readings of points the paper leaves open (block size 16, frozen-snapshot
 visibility inside a batch, the fully-cached cap, the hash itself, 1/sqrt(D)
