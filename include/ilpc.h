@@ -82,18 +82,73 @@ void ilpc_cache_destroy(ilpc_cache* cache);
 /* Forget every registered block and restart the block allocator at 0. */
 int ilpc_cache_reset(ilpc_cache* cache);
 
-/* stats[0] = registered keys, stats[1] = next free block id,
- * stats[2] = key capacity (7/8 of the slots), stats[3] = num_blocks. */
+/* stats[0] = registered keys, stats[1] = next free block id (for an LRU
+ * cache: blocks not on the free queue), stats[2] = key capacity (7/8 of the
+ * slots), stats[3] = num_blocks. */
 int ilpc_cache_stats(const ilpc_cache* cache, int64_t stats[4]);
 
 /* Record the current state so that ilpc_cache_rollback can return to it:
- * mark[0] = registered-key journal length, mark[1] = next free block id. */
+ * mark[0] = registered-key journal length, mark[1] = next free block id.
+ * ILPC_EUNSUP on an LRU cache (as is ilpc_cache_rollback). */
 int ilpc_cache_checkpoint(const ilpc_cache* cache, int64_t mark[2]);
 
 /* Undo every registration and block allocation made since `mark` was taken
  * (most recent first).  A mark from before a later reset or rollback past it
  * is rejected with ILPC_EINVAL. */
 int ilpc_cache_rollback(ilpc_cache* cache, const int64_t mark[2]);
+
+/*
+ * A prefix cache whose blocks have a lifecycle (section 2.1.2: KV blocks live
+ * in bounded GPU memory and are evicted least recently used first).  Matching
+ * and registration are those of ilpc_prefix_match; what differs is where
+ * block ids come from and when they return.  A block is
+ *   in use   -- held by at least one request not yet released (count > 0);
+ *   cached   -- held by none but its key still registered: a later request
+ *               can hit it; these blocks form the LRU list;
+ *   free     -- held by none and named by no key; on the free queue, which
+ *               starts as 0, 1, ..., num_blocks-1.
+ * ilpc_prefix_match on such a cache first pins every block the batch hits (in
+ * request order), then takes each new block from the front of the free queue,
+ * or, when the queue is empty, the head of the LRU list (least recently used),
+ * whose key is removed from the table.  It returns ILPC_ENOSPC, changing
+ * nothing, when the batch needs more new blocks than the free blocks plus the
+ * cached blocks it does not hit.  Without releases, ids come out exactly as
+ * from ilpc_cache_create's bump allocator.  The key capacity
+ * (7/8 * 2^table_log2_cap) must be >= num_blocks (ILPC_EINVAL otherwise), so
+ * ILPC_ETABLE never occurs.  Host memory only; the device pools are the
+ * caller's and are not touched.
+ */
+int ilpc_cache_create_lru(int32_t num_blocks, int32_t block_size, int32_t table_log2_cap,
+                          ilpc_cache** out);
+
+/*
+ * Requests finished: drop one hold on every block of each row of
+ * block_tables [host] int32 [B, max_blocks] (a row ends at its first -1), the
+ * rows as ilpc_prefix_match returned them.  Each row is released from its
+ * last block to its first; a block whose count reaches 0 goes to the tail of
+ * the LRU list if its key is registered, else to the back of the free queue
+ * (so a cached prompt loses its end before its start).  ILPC_EINVAL, changing
+ * nothing, if an id is out of range or a block would be released more often
+ * than it is held; ILPC_EUNSUP on a cache from ilpc_cache_create.
+ */
+int ilpc_cache_release(ilpc_cache* cache, const int32_t* block_tables, int32_t B,
+                       int32_t max_blocks);
+
+/* Mark cached blocks as just used: each id of block_ids [host] int32 [n] that
+ * names a cached block moves to the LRU tail, in order; ids of blocks in use
+ * or free, and -1 entries, change nothing.  ILPC_EINVAL (nothing changed) for
+ * an id outside [0, num_blocks) other than -1. */
+int ilpc_cache_touch(ilpc_cache* cache, const int32_t* block_ids, int32_t n);
+
+/* usage[0] = blocks in use, usage[1] = cached blocks, usage[2] = free blocks,
+ * usage[3] = evictions so far.  For a cache from ilpc_cache_create every
+ * allocated block counts as in use. */
+int ilpc_cache_usage(const ilpc_cache* cache, int64_t usage[4]);
+
+/* The cached blocks, least recently used first: writes min(max_ids, count)
+ * ids to block_ids [host] int32 [max_ids] and the count to *n_cached. */
+int ilpc_cache_lru_order(const ilpc_cache* cache, int32_t* block_ids, int32_t max_ids,
+                         int32_t* n_cached);
 
 /*
  * Block-level prefix matching of one batch (section 2.1.2).

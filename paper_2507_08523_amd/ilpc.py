@@ -44,6 +44,11 @@ _SIGS = [
     ("ilpc_paged_prefill_attn_cascade", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32,
                                                _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                                ctypes.c_size_t, _vp]),
+    ("ilpc_cache_create_lru", _i32, [_i32, _i32, _i32, ctypes.POINTER(_vp)]),
+    ("ilpc_cache_release", _i32, [_vp, _vp, _i32, _i32]),
+    ("ilpc_cache_touch", _i32, [_vp, _vp, _i32]),
+    ("ilpc_cache_usage", _i32, [_vp, _vp]),
+    ("ilpc_cache_lru_order", _i32, [_vp, _vp, _i32, ctypes.POINTER(_i32)]),
     ("ilpc_pair_create", _i32, [_i32, _i32, ctypes.POINTER(_vp)]),
     ("ilpc_pair_destroy", None, [_vp]),
     ("ilpc_pair_reset", _i32, [_vp]),
@@ -86,13 +91,18 @@ def _np_ptr(a: np.ndarray):
 
 
 class PrefixCache:
-    """Host prefix cache over a pool of ``num_blocks`` 16-token blocks."""
+    """Host prefix cache over a pool of ``num_blocks`` 16-token blocks.
 
-    def __init__(self, num_blocks: int, table_log2_cap: int = 20):
+    ``lru=True`` gives blocks a lifecycle (reference counts, a free queue and
+    least-recently-used eviction of cached blocks; see ``release``).
+    """
+
+    def __init__(self, num_blocks: int, table_log2_cap: int = 20, lru: bool = False):
         lib = load()
         h = ctypes.c_void_p()
-        _check(lib.ilpc_cache_create(num_blocks, BLOCK, table_log2_cap, ctypes.byref(h)))
-        self._h = h
+        create = lib.ilpc_cache_create_lru if lru else lib.ilpc_cache_create
+        _check(create(num_blocks, BLOCK, table_log2_cap, ctypes.byref(h)))
+        self._h, self.num_blocks, self.lru = h, num_blocks, lru
 
     def close(self):
         h, self._h = getattr(self, "_h", None), None
@@ -108,6 +118,31 @@ class PrefixCache:
         s = np.zeros(4, np.int64)
         _check(load().ilpc_cache_stats(self._h, _np_ptr(s)))
         return {"keys": int(s[0]), "next_block": int(s[1]), "capacity": int(s[2]), "num_blocks": int(s[3])}
+
+    def release(self, block_tables):
+        """Requests finished: release the blocks of each row (up to its first -1)."""
+        t = np.ascontiguousarray(block_tables, dtype=np.int32)
+        if t.ndim != 2:
+            raise ILPCError(EINVAL, "release: block_tables must be [B, max_blocks]")
+        if t.shape[0]:
+            _check(load().ilpc_cache_release(self._h, _np_ptr(t), t.shape[0], t.shape[1]))
+
+    def touch(self, block_ids):
+        ids = np.ascontiguousarray(block_ids, dtype=np.int32).reshape(-1)
+        _check(load().ilpc_cache_touch(self._h, _np_ptr(ids), ids.size))
+
+    def usage(self) -> tuple:
+        """(blocks in use, cached blocks, free blocks, evictions so far)."""
+        u = np.zeros(4, np.int64)
+        _check(load().ilpc_cache_usage(self._h, _np_ptr(u)))
+        return tuple(int(x) for x in u)
+
+    def lru_order(self) -> list:
+        """Cached blocks, least recently used first."""
+        out = np.zeros(max(self.num_blocks, 1), np.int32)
+        n = ctypes.c_int32()
+        _check(load().ilpc_cache_lru_order(self._h, _np_ptr(out), out.size, ctypes.byref(n)))
+        return out[:n.value].tolist()
 
     def checkpoint(self) -> np.ndarray:
         m = np.zeros(2, np.int64)

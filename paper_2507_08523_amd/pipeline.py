@@ -37,13 +37,13 @@ class PagedPrefixCache:
     """Prefix cache (host) + paged K/V pools (device) for one attention layer."""
 
     def __init__(self, n_kv_heads: int, head_dim: int, num_blocks: int, max_blocks: int,
-                 max_batch: int, table_log2_cap: int = 20, device="cuda"):
+                 max_batch: int, table_log2_cap: int = 20, device="cuda", lru: bool = False):
         import torch
 
         self.n_kv_heads, self.head_dim = n_kv_heads, head_dim
         self.num_blocks, self.max_blocks, self.max_batch = num_blocks, max_blocks, max_batch
         self.device = torch.device(device)
-        self.cache = ilpc.PrefixCache(num_blocks, table_log2_cap)
+        self.cache = ilpc.PrefixCache(num_blocks, table_log2_cap, lru=lru)
         self.k_pool, self.v_pool = ilpc.alloc_pools(num_blocks, n_kv_heads, head_dim, self.device)
         n = max_batch * max_blocks + 3 * max_batch + 1
         self._host = [torch.empty(n, dtype=torch.int32, pin_memory=True) for _ in range(2)]
@@ -55,6 +55,15 @@ class PagedPrefixCache:
     def match(self, prompts=None, reserve=None, flags=0, packed=None):
         return self.cache.match(prompts, reserve=reserve, max_blocks=self.max_blocks, flags=flags,
                                 packed=packed)[:2]
+
+    def release(self, tables):
+        """Requests finished (LRU caches): their blocks become cached or free.
+
+        The caller orders this after the device work that reads those blocks;
+        a block taken again by a later batch is only rewritten by work queued
+        after it on the same stream.
+        """
+        self.cache.release(tables)
 
     # -- host -> device -----------------------------------------------------
     def upload(self, tables: np.ndarray, cu_q: np.ndarray, seq_lens: np.ndarray,
@@ -165,22 +174,30 @@ def pair_refine_stream(stream, capacity: int, batch: int):
     return out_t, out_d, pmc
 
 
-def stream_hit_rate(prompts, batch: int, table_log2_cap: int = 20) -> dict:
+def stream_hit_rate(prompts, batch: int, pool_blocks: int | None = None) -> dict:
     """Prefix-cache hit rate of a request stream served ``batch`` prompts at a time.
 
-    Every batch is matched against the blocks of all earlier batches (the pool
-    holds the whole stream, nothing is evicted).  The rate is cached prompt
-    tokens over prompt tokens.
+    Without ``pool_blocks`` the pool holds the whole stream and nothing is
+    evicted.  With it, the pool has that many blocks: each batch's requests
+    finish before the next batch arrives, and cached blocks are evicted least
+    recently used first.  The rate is cached prompt tokens over prompt tokens.
     """
-    n_blocks = sum(-(-len(p) // BLOCK) for p in prompts) + 1
-    cache = ilpc.PrefixCache(n_blocks, table_log2_cap)
+    lru = pool_blocks is not None
+    n_blocks = pool_blocks if lru else sum(-(-len(p) // BLOCK) for p in prompts) + 1
+    log2cap = max(4, int(np.ceil(np.log2(n_blocks * 8 / 7 + 1))) + 1)
+    cache = ilpc.PrefixCache(n_blocks, log2cap, lru=lru)
     cached = 0
     for s in range(0, len(prompts), batch):
-        c, _, _ = cache.match(prompts[s:s + batch])
+        c, t, _ = cache.match(prompts[s:s + batch])
         cached += int(c.sum())
+        if lru:
+            cache.release(t)
     total = int(sum(len(p) for p in prompts))
+    out = {"cached_tokens": cached, "prompt_tokens": total, "hit_rate": cached / total}
+    if lru:
+        out["evictions"] = cache.usage()[3]
     cache.close()
-    return {"cached_tokens": cached, "prompt_tokens": total, "hit_rate": cached / total}
+    return out
 
 
 def pool_blocks_needed(wl) -> int:

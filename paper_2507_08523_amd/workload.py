@@ -181,6 +181,33 @@ def icl_stream(spec: WorkloadSpec | str) -> IclStream:
                      queries=queries)
 
 
+def cache_op_stream(seed: int, n_steps: int = 60, n_pieces: int = 5):
+    """Seeded operations on a prefix cache with a block lifecycle.
+
+    ("match", prompts): 1-3 prompts, each 1-3 shared pieces of 8-49 tokens in a
+    random order plus a private tail of 1-19 tokens; ("release", u): finish a
+    fraction u of the requests still held; ("touch", ids): 4 block ids in
+    [-1, 40).
+    """
+    rng = np.random.default_rng(seed)
+    pieces = [rng.integers(0, VOCAB, int(rng.integers(8, 50))).astype(np.int32) for _ in range(n_pieces)]
+    ops = []
+    for _ in range(n_steps):
+        u = rng.random()
+        if u < 0.55:
+            prompts = []
+            for _ in range(int(rng.integers(1, 4))):
+                order = rng.permutation(n_pieces)[:int(rng.integers(1, 4))]
+                tail = rng.integers(0, VOCAB, int(rng.integers(1, 20))).astype(np.int32)
+                prompts.append(np.concatenate([pieces[i] for i in order] + [tail]))
+            ops.append(("match", prompts))
+        elif u < 0.9:
+            ops.append(("release", float(rng.random())))
+        else:
+            ops.append(("touch", [int(x) for x in rng.integers(-1, 40, 4)]))
+    return ops
+
+
 def scaled_spec(name: str, n_prompts: int, **over) -> WorkloadSpec:
     """A named workload with fewer prompts (same per-prompt structure)."""
     base = SPECS[name]

@@ -15,6 +15,7 @@ import pytest
 
 from oracle.lifecycle_ref import LruPrefixCacheRef
 from oracle.prefix_ref import BLOCK, OracleError, PrefixCacheRef
+from paper_2507_08523_amd.workload import cache_op_stream
 
 
 def _ar(a, b):
@@ -162,27 +163,6 @@ class _ExactPrefixModel:
         return sorted(self.stamp, key=self.stamp.get)
 
 
-def random_lifecycle_stream(seed, n_steps=60):
-    """Batches of prompts sharing pieces, releases and touches; yields ops."""
-    rng = np.random.default_rng(seed)
-    pieces = [rng.integers(0, 32000, int(rng.integers(8, 50))).astype(np.int32) for _ in range(5)]
-    ops = []
-    for _ in range(n_steps):
-        u = rng.random()
-        if u < 0.55:
-            prompts = []
-            for _ in range(int(rng.integers(1, 4))):
-                order = rng.permutation(5)[:int(rng.integers(1, 4))]
-                tail = rng.integers(0, 32000, int(rng.integers(1, 20))).astype(np.int32)
-                prompts.append(np.concatenate([pieces[i] for i in order] + [tail]))
-            ops.append(("match", prompts))
-        elif u < 0.9:
-            ops.append(("release", float(rng.random())))
-        else:
-            ops.append(("touch", [int(x) for x in rng.integers(-1, 40, 4)]))
-    return ops
-
-
 @pytest.mark.parametrize("seed", range(6))
 def test_random_streams_against_exact_prefix_model(seed):
     n_blocks, max_blocks = 40, 12
@@ -190,7 +170,7 @@ def test_random_streams_against_exact_prefix_model(seed):
     rng = np.random.default_rng(100 + seed)
     live = []                      # tables of requests not yet released
     n_hits = n_refused = 0
-    for op, arg in random_lifecycle_stream(seed):
+    for op, arg in cache_op_stream(seed):
         if op == "match":
             got = brute.match(arg, max_blocks)
             if got is None:
