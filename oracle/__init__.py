@@ -19,6 +19,8 @@ InferLog paper (arXiv 2507.08523) it follows.
   and the ICL table (sections 3.2.1 and 3.2.2).
 * ``lifecycle_ref`` -- the prefix cache with reference-counted blocks and
   least-recently-used eviction (section 2.1.2).
+* ``rope_ref``    -- rotary position embedding of the new tokens' keys and
+  queries at their absolute positions (section 2.1.2; RoFormer's rotation).
 
 Readings of points the paper leaves open (block size 16, frozen-snapshot
 visibility inside a batch, the fully-cached cap, the hash itself, 1/sqrt(D)
