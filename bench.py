@@ -23,6 +23,12 @@ sample of the same workload on the host cores.
 ``--cascade`` runs the prefill attention split at the prefix every prompt of
 the batch shares (ilpc_paged_prefill_attn_cascade).
 
+``--rope BASE`` rotates the new tokens' K and Q at their positions inside the
+append (ilpc_rope_kv_append; the warm prefix is rotated the same way).
+``--chunk-tokens N`` runs the prefill as scheduler steps of at most N new
+tokens (append + attention per step); the attention timing and ``roofline``
+then cover all steps.
+
 ICL stream workloads (``icl_llama8b``): 2000 log-parsing requests whose
 demonstrations a selector picks with hot templates.  Before the timed steps the
 whole stream passes the ICL table (prefix-aware refinement, host C++) in
@@ -165,6 +171,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-pair", action="store_true",
                     help="ICL stream workloads: serve the selector's demonstration order unrefined")
+    ap.add_argument("--chunk-tokens", type=int, default=0,
+                    help="prefill in scheduler steps of at most this many new tokens (0: one pass)")
+    ap.add_argument("--rope", type=float, default=0.0, metavar="BASE",
+                    help="rotate new K and Q with RoPE of this base inside the append (0: off)")
     ap.add_argument("--cascade", action="store_true",
                     help="split the prefill attention at the prefix every prompt shares")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -178,8 +188,8 @@ def main():
     import torch
 
     from paper_2507_08523_amd import ilpc, workload
-    from paper_2507_08523_amd.pipeline import (PagedPrefixCache, max_blocks_of, pool_blocks_needed,
-                                               shared_prefix_len)
+    from paper_2507_08523_amd.pipeline import (PagedPrefixCache, chunk_schedule, max_blocks_of,
+                                               pool_blocks_needed, rope_inv_freq, shared_prefix_len)
 
     ilpc.load()
     dev = torch.device("cuda:0")
@@ -204,11 +214,20 @@ def main():
     pc = PagedPrefixCache(sp.n_kv_heads, sp.head_dim, pool_blocks_needed(wl), max_blocks_of(wl),
                           max(len(wl.prompts), len(wl.warm), 1), 20, dev)
 
+    if args.cascade and (args.rope or args.chunk_tokens):
+        print("--cascade does not combine with --rope or --chunk-tokens", file=sys.stderr)
+        sys.exit(2)
+    inv_freq = torch.from_numpy(rope_inv_freq(sp.head_dim, args.rope)).to(dev) if args.rope else None
+
     # warm pass (untimed): registers the shared prefix blocks and their K/V
     if wl.warm:
         c, t = pc.match(wl.warm)
         rows = wl.packed_warm(c)
-        pc.append(pc.upload_prefill(c, t, [len(p) for p in wl.warm]), rows["k_new"], rows["v_new"])
+        b = pc.upload_prefill(c, t, [len(p) for p in wl.warm])
+        if args.rope:
+            pc.append_rope(b, rows["k_new"], rows["v_new"], inv_freq)
+        else:
+            pc.append(b, rows["k_new"], rows["v_new"])
         torch.cuda.synchronize()
         del rows
 
@@ -225,6 +244,8 @@ def main():
     rows = wl.packed_suffix(cached)
     q, k_new, v_new = rows["q"], rows["k_new"], rows["v_new"]
     out = torch.empty_like(q)
+    q_rot = torch.empty_like(q) if args.rope else None
+    n_chunks = len(chunk_schedule(wl.seq_lens - cached, args.chunk_tokens)) if args.chunk_tokens else 1
     shared_len, cascade_ws = 0, None
     if args.cascade:
         shared_len = shared_prefix_len(cached, tables)
@@ -237,6 +258,7 @@ def main():
     L = wl.seq_lens.astype(np.int32)
     dec_in = [wl.decode_inputs(s) for s in range(dec)]
     dec_out = [torch.empty_like(d["q"]) for d in dec_in]
+    dec_rot = [torch.empty_like(d["q"]) for d in dec_in] if args.rope else None
     cu_dec = np.arange(len(L) + 1, dtype=np.int32)
     work = workload_work(wl, cached)
     n_tokens = work["query_tokens"] + dec * len(L)
@@ -250,24 +272,37 @@ def main():
         h0 = time.perf_counter()
         m = pc.cache.checkpoint()
         c, t = pc.match(packed=(tokens, cu_tok), reserve=reserve)
-        b = pc.upload_prefill(c, t, L, stream)
+        b = None if args.chunk_tokens else pc.upload_prefill(c, t, L, stream)
         pc.cache.rollback(m)
         host_s.append(time.perf_counter() - h0)
         e[0].record(stream)
-        pc.append(b, k_new, v_new, stream)
-        e[1].record(stream)
-        if args.cascade:
-            pc.attend_cascade(b, q, out, sp.scale, shared_len, cascade_ws, stream)
+        if args.chunk_tokens:   # appends and attention interleave, chunk by chunk
+            e[1].record(stream)
+            pc.prefill_chunked(c, t, L, q, k_new, v_new, out, sp.scale, args.chunk_tokens, stream,
+                               inv_freq, q_rot)
         else:
-            pc.attend(b, q, out, sp.scale, stream)
+            if args.rope:
+                pc.append_rope(b, k_new, v_new, inv_freq, q, q_rot, stream)
+            else:
+                pc.append(b, k_new, v_new, stream)
+            e[1].record(stream)
+            if args.cascade:
+                pc.attend_cascade(b, q, out, sp.scale, shared_len, cascade_ws, stream)
+            else:
+                pc.attend(b, q_rot if args.rope else q, out, sp.scale, stream)
         e[2].record(stream)
         for s in range(dec):
             bd = pc.upload(t, cu_dec, L + s + 1, L + s, stream)
-            pc.append(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], stream)
-            if args.cascade:
-                pc.attend_cascade(bd, dec_in[s]["q"], dec_out[s], sp.scale, shared_len, decode_ws, stream)
+            qd = dec_in[s]["q"]
+            if args.rope:
+                pc.append_rope(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], inv_freq, qd, dec_rot[s], stream)
+                qd = dec_rot[s]
             else:
-                pc.attend(bd, dec_in[s]["q"], dec_out[s], sp.scale, stream)
+                pc.append(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], stream)
+            if args.cascade:
+                pc.attend_cascade(bd, qd, dec_out[s], sp.scale, shared_len, decode_ws, stream)
+            else:
+                pc.attend(bd, qd, dec_out[s], sp.scale, stream)
         e[3].record(stream)
         return c
 
@@ -318,8 +353,11 @@ def main():
                    "query_tokens": work["query_tokens"], "decode_steps": dec,
                    "cached_fraction": round(float(cached.sum() / wl.seq_lens.sum()), 4),
                    **({"cascade_shared_len": shared_len} if args.cascade else {}),
+                   **({"chunk_tokens": args.chunk_tokens, "chunks": n_chunks} if args.chunk_tokens else {}),
+                   **({"rope_base": args.rope} if args.rope else {}),
                    **(icl or {})},
-        "roofline": roof,
+        "roofline": {**roof, **({"scope": f"all {n_chunks} chunked steps: appends, attention and the "
+                                         "host's per-step metadata copies"} if args.chunk_tokens else {})},
         "attn": {"launch_us": round(attn_ms * 1e3, 2), "tflops": round(tflops, 2),
                  "logical_gbs": round(gbs, 1), "flops": work["flops"], "logical_bytes": work["logical_bytes"],
                  "kernel_sha": kernel_source_sha()},

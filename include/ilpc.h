@@ -206,6 +206,36 @@ int ilpc_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_poo
                    int32_t max_blocks, const int32_t* cu_new, const int32_t* start_pos, int32_t B,
                    int32_t max_new, int32_t Hkv, int32_t D, int32_t block_size, void* stream);
 
+/*
+ * Rotary position embedding fused into the K/V append (section 2.1.2: the
+ * stored KV carries each token's position).  Same rows, pools, tables and
+ * bounds rules as ilpc_kv_append, plus:
+ *
+ * q        [device] bf16 [cu_new[B], Hq, D] or NULL  query rows of the same
+ *                   tokens (packed like k_new)
+ * q_out    [device] bf16 [cu_new[B], Hq, D] or NULL  rotated queries; may be
+ *                   q itself (in place); NULL exactly when q is NULL
+ * inv_freq [device] fp32 [D/2]  angle per position of dimension pair i
+ *                   (base^(-2i/D) for plain RoPE; any scaled variant the
+ *                   model uses is the caller's table)
+ *
+ * Row t of request r sits at position p = start_pos[r] + t.  For i < D/2 the
+ * pair (x_i, x_{i+D/2}) of its K row and of each of its Q rows becomes
+ *   (x_i cos a - x_{i+D/2} sin a,  x_{i+D/2} cos a + x_i sin a),
+ *   a = fl32(p * inv_freq[i]),
+ * computed in fp32 from the bf16 inputs and rounded to bf16 (nearest even);
+ * the rotated K row is stored in the pool, V unchanged.  Q rows are rotated
+ * even where the block id is outside [0, num_blocks) (only K/V are skipped);
+ * rows past max_new or whose logical block is >= max_blocks are not written.
+ * Supported: D in {64, 128}, Hq % Hkv == 0, Hq / Hkv <= 64.
+ */
+int ilpc_rope_kv_append(const uint16_t* q, uint16_t* q_out, int32_t Hq, const uint16_t* k_new,
+                        const uint16_t* v_new, uint16_t* k_pool, uint16_t* v_pool,
+                        int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                        const int32_t* cu_new, const int32_t* start_pos, int32_t B,
+                        int32_t max_new, int32_t Hkv, int32_t D, int32_t block_size,
+                        const float* inv_freq, void* stream);
+
 /* Bytes of device workspace ilpc_paged_prefill_attn needs for these sizes
  * (currently 64 for every shape: the counters of its work queues). */
 int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,

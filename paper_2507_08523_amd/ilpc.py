@@ -36,6 +36,8 @@ _SIGS = [
     ("ilpc_prefix_match", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _u32, _vp, _vp, _vp]),
     ("ilpc_kv_append", _i32, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
                               _i32, _i32, _vp]),
+    ("ilpc_rope_kv_append", _i32, [_vp, _vp, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32,
+                                   _i32, _i32, _i32, _i32, _vp, _vp]),
     ("ilpc_attn_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
     ("ilpc_paged_prefill_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
                                        _i32, _i32, _i32, _f32, _vp, _vp, ctypes.c_size_t, _vp]),
@@ -280,6 +282,39 @@ def kv_append(k_new, v_new, k_pool, v_pool, block_tables, cu_new, start_pos, max
             _dev(cu_new, torch.int32, "cu_new", 1), _dev(start_pos, torch.int32, "start_pos", 1),
             B, int(max_new), Hkv, D, bs, _stream(stream))
     _check(load().ilpc_kv_append(*args))
+
+
+def rope_kv_append(q, q_out, k_new, v_new, k_pool, v_pool, block_tables, cu_new, start_pos, max_new: int,
+                   inv_freq, stream=None):
+    """Rotate new K (and Q, if given) at their positions and write K/V into the pools.
+
+    q, q_out: [total, Hq, D] bf16 or both None (q_out may be q); inv_freq: fp32 [D/2].
+    """
+    import torch
+
+    NB, Hkv, bs, D = k_pool.shape
+    if v_pool.shape != (NB, Hkv, D, bs) or k_new.shape[1:] != (Hkv, D) or v_new.shape != k_new.shape:
+        raise ILPCError(EINVAL, "rope_kv_append: inconsistent K/V/pool shapes")
+    if (q is None) != (q_out is None):
+        raise ILPCError(EINVAL, "rope_kv_append: q and q_out must both be given or both be None")
+    Hq = Hkv
+    if q is not None:
+        Hq = q.shape[1]
+        if q.shape != (k_new.shape[0], Hq, D) or q_out.shape != q.shape:
+            raise ILPCError(EINVAL, "rope_kv_append: q / q_out must be [total, Hq, D] like k_new")
+    if inv_freq.shape != (D // 2,):
+        raise ILPCError(EINVAL, "rope_kv_append: inv_freq must be [D/2]")
+    B = cu_new.shape[0] - 1
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or start_pos.shape[0] != B:
+        raise ILPCError(EINVAL, "rope_kv_append: inconsistent batch shapes")
+    qp = _dev(q, torch.bfloat16, "q", 3) if q is not None else None
+    qo = _dev(q_out, torch.bfloat16, "q_out", 3) if q_out is not None else None
+    args = (qp, qo, Hq, _dev(k_new, torch.bfloat16, "k_new", 3), _dev(v_new, torch.bfloat16, "v_new", 3),
+            _dev(k_pool, torch.bfloat16, "k_pool", 4), _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
+            _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],
+            _dev(cu_new, torch.int32, "cu_new", 1), _dev(start_pos, torch.int32, "start_pos", 1),
+            B, int(max_new), Hkv, D, bs, _dev(inv_freq, torch.float32, "inv_freq", 1), _stream(stream))
+    _check(load().ilpc_rope_kv_append(*args))
 
 
 def attn_workspace_bytes(B, max_q_len, Hq, Hkv, D) -> int:

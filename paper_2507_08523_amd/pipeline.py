@@ -50,6 +50,7 @@ class PagedPrefixCache:
         self._host_ev = [None, None]
         self._flip = 0
         self._dev = torch.empty(n, dtype=torch.int32, device=self.device)
+        self._steps_host = self._steps_dev = self._steps_ev = None
 
     # -- host ---------------------------------------------------------------
     def match(self, prompts=None, reserve=None, flags=0, packed=None):
@@ -100,6 +101,52 @@ class PagedPrefixCache:
                            max_q_len=int(q_lens.max()) if B else 0, total_q=int(cu_q[-1]) if B else 0,
                            B=B)
 
+    def upload_steps(self, steps, stream=None) -> list:
+        """Metadata of several batches, ``steps`` = [(tables, cu_q, seq_lens, start_pos)],
+        staged together and sent with one async H2D copy; returns a DeviceBatch each.
+
+        The staging buffers grow on demand (a first call may allocate) and are
+        reused: a later call first waits for the copy that last read them.
+        """
+        import torch
+
+        stream = stream or torch.cuda.current_stream(self.device)
+        sizes = [int(t.shape[0]) * self.max_blocks + 3 * int(t.shape[0]) + 1 for (t, _, _, _) in steps]
+        n = int(sum(sizes))
+        if self._steps_host is None or self._steps_host.numel() < n:
+            if self._steps_ev is not None:
+                self._steps_ev.synchronize()
+            cap = max(n, 2 * (self._steps_host.numel() if self._steps_host is not None else 0))
+            self._steps_host = torch.empty(cap, dtype=torch.int32, pin_memory=True)
+            self._steps_dev = torch.empty(cap, dtype=torch.int32, device=self.device)
+        elif self._steps_ev is not None:
+            self._steps_ev.synchronize()
+        h = self._steps_host.numpy()
+        out, o = [], 0
+        for (tables, cu_q, seq_lens, start_pos), size in zip(steps, sizes):
+            B = int(tables.shape[0])
+            if tables.shape[1] != self.max_blocks:
+                raise ilpc.ILPCError(ilpc.EINVAL, "upload_steps: block table width differs from max_blocks")
+            nbt = B * self.max_blocks
+            h[o:o + nbt] = tables.reshape(-1)
+            h[o + nbt:o + nbt + B + 1] = cu_q
+            h[o + nbt + B + 1:o + nbt + 2 * B + 1] = seq_lens
+            h[o + nbt + 2 * B + 1:o + size] = start_pos
+            d = self._steps_dev
+            q_lens = np.diff(np.asarray(cu_q, dtype=np.int64))
+            out.append(DeviceBatch(block_tables=d[o:o + nbt].view(B, self.max_blocks),
+                                   cu_q=d[o + nbt:o + nbt + B + 1],
+                                   seq_lens=d[o + nbt + B + 1:o + nbt + 2 * B + 1],
+                                   start_pos=d[o + nbt + 2 * B + 1:o + size],
+                                   max_q_len=int(q_lens.max()) if B else 0,
+                                   total_q=int(cu_q[-1]) if B else 0, B=B))
+            o += size
+        with torch.cuda.stream(stream):
+            self._steps_dev[:n].copy_(self._steps_host[:n], non_blocking=True)
+            self._steps_ev = torch.cuda.Event()
+            self._steps_ev.record(stream)
+        return out
+
     def upload_prefill(self, cached_len, tables, seq_lens, stream=None) -> DeviceBatch:
         """Metadata of a prefill: queries are positions cached_len[r]..seq_lens[r]-1."""
         seq_lens = np.asarray(seq_lens, dtype=np.int32)
@@ -112,6 +159,50 @@ class PagedPrefixCache:
     def append(self, batch: DeviceBatch, k_new, v_new, stream=None):
         ilpc.kv_append(k_new, v_new, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
                        batch.start_pos, batch.max_q_len, stream)
+
+    def append_rope(self, batch: DeviceBatch, k_new, v_new, inv_freq, q=None, q_out=None, stream=None):
+        """kv_append with K (and Q into q_out) rotated at their absolute positions."""
+        ilpc.rope_kv_append(q, q_out, k_new, v_new, self.k_pool, self.v_pool, batch.block_tables,
+                            batch.cu_q, batch.start_pos, batch.max_q_len, inv_freq, stream)
+
+    def prefill_chunked(self, cached_len, tables, seq_lens, q, k_new, v_new, out, scale: float,
+                        budget: int, stream=None, inv_freq=None, q_rot=None):
+        """Prefill of a matched batch in scheduler steps of at most ``budget`` tokens.
+
+        q, k_new, v_new, out: the batch's suffix rows, packed request by
+        request (as for a single pass).  Step s covers packed rows
+        [s * budget, (s + 1) * budget): the rest of one request, whole
+        requests, the head of another (first come, first served).  Each step
+        appends its rows' K/V and attends its queries over every key up to its
+        last row.  The metadata of all steps goes to the device in one copy,
+        so a step costs the host two launches.  With ``inv_freq`` the append
+        also rotates K and Q (into ``q_rot``, which attention then reads).
+        Returns the number of steps.
+        """
+        cached_len = np.asarray(cached_len, dtype=np.int64)
+        q_lens = np.asarray(seq_lens, dtype=np.int64) - cached_len
+        steps = chunk_schedule(q_lens, budget)
+        meta = []
+        for step in steps:
+            rs = [r for (r, _, _) in step]
+            n = np.array([m for (_, _, m) in step], np.int64)
+            off = np.array([o for (_, o, _) in step], np.int64)
+            start = cached_len[rs] + off
+            cu = np.zeros(len(step) + 1, np.int32)
+            cu[1:] = np.cumsum(n)
+            meta.append((np.ascontiguousarray(tables[rs]), cu, (start + n).astype(np.int32),
+                         start.astype(np.int32)))
+        row = 0
+        for b in self.upload_steps(meta, stream):
+            rows = slice(row, row + b.total_q)
+            if inv_freq is None:
+                self.append(b, k_new[rows], v_new[rows], stream)
+                self.attend(b, q[rows], out[rows], scale, stream)
+            else:
+                self.append_rope(b, k_new[rows], v_new[rows], inv_freq, q[rows], q_rot[rows], stream)
+                self.attend(b, q_rot[rows], out[rows], scale, stream)
+            row += b.total_q
+        return len(steps)
 
     def attend(self, batch: DeviceBatch, q, out, scale: float, stream=None):
         ilpc.paged_prefill_attn(q, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
@@ -133,6 +224,38 @@ class PagedPrefixCache:
         ws = torch.empty(n, dtype=torch.uint8, device=self.device)
         ws[:128].zero_()
         return ws
+
+
+def chunk_schedule(q_lens, budget: int):
+    """Scheduler steps of at most ``budget`` new tokens (max-num-batched-tokens).
+
+    First come, first served over the batch's requests in order: a step takes
+    what is left of the current request, then the next requests, and cuts the
+    last one it reaches.  Returns, per step, a list of (request, offset into
+    its new tokens, count); requests with no new tokens are skipped.
+    """
+    if budget < 1:
+        raise ilpc.ILPCError(ilpc.EINVAL, "chunk_schedule: budget < 1")
+    steps, cur, room = [], [], budget
+    for r, n in enumerate(np.asarray(q_lens, dtype=np.int64).tolist()):
+        off = 0
+        while off < n:
+            take = min(n - off, room)
+            cur.append((r, off, take))
+            off += take
+            room -= take
+            if room == 0:
+                steps.append(cur)
+                cur, room = [], budget
+    if cur:
+        steps.append(cur)
+    return steps
+
+
+def rope_inv_freq(head_dim: int, base: float):
+    """fp32 angle table of plain RoPE: base^(-2i/D), i < D/2 (a model constant,
+    passed to the append kernel as data)."""
+    return (base ** (-np.arange(0, head_dim, 2, dtype=np.float64) / head_dim)).astype(np.float32)
 
 
 def shared_prefix_len(cached_len, block_tables) -> int:
