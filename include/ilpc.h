@@ -236,6 +236,22 @@ int ilpc_rope_kv_append(const uint16_t* q, uint16_t* q_out, int32_t Hq, const ui
                         int32_t max_new, int32_t Hkv, int32_t D, int32_t block_size,
                         const float* inv_freq, void* stream);
 
+/*
+ * Decode-shaped paged attention (section 2.1.2: each generated token attends
+ * to the cached KV of its whole context): the same operation, arguments,
+ * layouts and bounds rules as ilpc_paged_prefill_attn, for batches whose
+ * max_q_len * (Hq / Hkv) <= 32 (ILPC_EUNSUP otherwise), with no workspace.
+ * One wave per (request, kv head) streams that request's K/V blocks from the
+ * pools; results agree with ilpc_paged_prefill_attn to the attention
+ * tolerance, not bit for bit.  ilpc_paged_prefill_attn takes this path by
+ * itself for such batches when B * Hkv >= the device's compute units.
+ */
+int ilpc_paged_decode_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                           int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                           const int32_t* cu_q, const int32_t* seq_lens, int32_t B, int32_t max_q_len,
+                           int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size, float softmax_scale,
+                           uint16_t* out, void* stream);
+
 /* Bytes of device workspace ilpc_paged_prefill_attn needs for these sizes
  * (currently 64 for every shape: the counters of its work queues). */
 int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,

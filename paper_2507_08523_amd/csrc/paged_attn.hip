@@ -50,6 +50,7 @@ constexpr int kKeys = 64;                     // keys per tile
 constexpr int kTileBlocks = kKeys / kBlock;
 constexpr int kStages = 4;                    // K/V tiles resident in the LDS ring
 constexpr int kMaxGroup = 64;                 // largest Hq / Hkv accepted
+constexpr int kDecodeCols = 32;               // query columns the decode kernel takes per request
 
 // LDS row that holds tile key k.  Inside every 16 keys the groups [4,8) and
 // [8,12) trade places, so that MFMA row m of S^T carries key sigma(m) and the
@@ -796,11 +797,32 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
   if (!workspace || workspace_bytes < kQueueWords * sizeof(unsigned) || !aligned16(workspace))
     return ilpc::set_error(ILPC_EINVAL, "%s: workspace must be %zu bytes, 16-byte aligned", fn,
                            kQueueWords * sizeof(unsigned));
+  // Decode-shaped batches with enough (request, kv head) pairs to fill the
+  // chip go to the one-wave-per-pair kernel.
+  if (int64_t(max_q_len) * (Hq / Hkv) <= kDecodeCols && int64_t(B) * Hkv >= device_cus())
+    return ilpc::launch_decode_attn(q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                                    max_q_len, Hq, Hkv, D, softmax_scale * 1.4426950408889634f, out, stream);
   const int64_t col_tiles = (int64_t(max_q_len) * (Hq / Hkv) + kCols - 1) / kCols;
   return launch_attn<kFull>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
                             Hq, Hkv, D, col_tiles, softmax_scale * 1.4426950408889634f, out,
                             static_cast<unsigned*>(workspace), 0, nullptr, nullptr, 0,
                             static_cast<hipStream_t>(stream));
+}
+
+extern "C" int ilpc_paged_decode_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                                     int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                                     const int32_t* cu_q, const int32_t* seq_lens, int32_t B, int32_t max_q_len,
+                                     int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size,
+                                     float softmax_scale, uint16_t* out, void* stream) {
+  static const char* fn = "ilpc_paged_decode_attn";
+  int rc = check_attn_args(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                           max_q_len, Hq, Hkv, D, block_size, softmax_scale, out);
+  if (rc != ILPC_OK || B == 0 || max_q_len == 0) return rc;
+  if (int64_t(max_q_len) * (Hq / Hkv) > kDecodeCols)
+    return ilpc::set_error(ILPC_EUNSUP, "%s: max_q_len * Hq / Hkv = %lld > %d", fn,
+                           (long long)max_q_len * (Hq / Hkv), kDecodeCols);
+  return ilpc::launch_decode_attn(q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                                  max_q_len, Hq, Hkv, D, softmax_scale * 1.4426950408889634f, out, stream);
 }
 
 extern "C" int ilpc_attn_cascade_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv,

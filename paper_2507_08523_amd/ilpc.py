@@ -41,6 +41,8 @@ _SIGS = [
     ("ilpc_attn_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
     ("ilpc_paged_prefill_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
                                        _i32, _i32, _i32, _f32, _vp, _vp, ctypes.c_size_t, _vp]),
+    ("ilpc_paged_decode_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
+                                      _i32, _i32, _i32, _f32, _vp, _vp]),
     ("ilpc_attn_cascade_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32,
                                                  ctypes.POINTER(ctypes.c_size_t)]),
     ("ilpc_paged_prefill_attn_cascade", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32,
@@ -371,6 +373,28 @@ def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_le
             int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3),
             ws_ptr, ws_bytes, _stream(stream))
     _check(load().ilpc_paged_prefill_attn(*args))
+
+
+def paged_decode_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_len: int, scale: float, out,
+                      stream=None):
+    """The decode kernel alone (max_q_len * Hq / Hkv <= 32): same semantics as
+    paged_prefill_attn, which picks it by itself for such batches when they
+    have at least one (request, kv head) pair per compute unit."""
+    import torch
+
+    NB, Hkv, bs, D = k_pool.shape
+    total, Hq, Dq = q.shape
+    B = cu_q.shape[0] - 1
+    if Dq != D or v_pool.shape != (NB, Hkv, D, bs) or out.shape != q.shape:
+        raise ILPCError(EINVAL, "paged_decode_attn: inconsistent Q/K/V/out shapes")
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ILPCError(EINVAL, "paged_decode_attn: inconsistent batch shapes")
+    args = (_dev(q, torch.bfloat16, "q", 3), _dev(k_pool, torch.bfloat16, "k_pool", 4),
+            _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
+            _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],
+            _dev(cu_q, torch.int32, "cu_q", 1), _dev(seq_lens, torch.int32, "seq_lens", 1), B,
+            int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3), _stream(stream))
+    _check(load().ilpc_paged_decode_attn(*args))
 
 
 def attn_cascade_workspace_bytes(B, max_q_len, Hq, Hkv, D) -> int:
