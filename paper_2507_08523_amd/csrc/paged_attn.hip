@@ -36,7 +36,6 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -283,7 +282,6 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   }
   const int my_blk = wave >> 1;
   const bool lag = wave >= kWaves / 2;
-  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
 
   if (tid == 0) {
     s_item[0] = fetch();
