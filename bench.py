@@ -27,7 +27,9 @@ the batch shares (ilpc_paged_prefill_attn_cascade).
 append (ilpc_rope_kv_append; the warm prefix is rotated the same way).
 ``--chunk-tokens N`` runs the prefill as scheduler steps of at most N new
 tokens (append + attention per step); the attention timing and ``roofline``
-then cover all steps.
+then cover all steps.  ``--graph`` (decode workloads) captures the 32 decode
+steps once as a HIP graph with all their metadata on the device, and every
+timed step replays it.
 
 ICL stream workloads (``icl_llama8b``): 2000 log-parsing requests whose
 demonstrations a selector picks with hot templates.  Before the timed steps the
@@ -175,6 +177,8 @@ def main():
                     help="prefill in scheduler steps of at most this many new tokens (0: one pass)")
     ap.add_argument("--rope", type=float, default=0.0, metavar="BASE",
                     help="rotate new K and Q with RoPE of this base inside the append (0: off)")
+    ap.add_argument("--graph", action="store_true",
+                    help="decode workloads: replay the decode steps as one captured HIP graph")
     ap.add_argument("--cascade", action="store_true",
                     help="split the prefill attention at the prefix every prompt shares")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -188,7 +192,7 @@ def main():
     import torch
 
     from paper_2507_08523_amd import ilpc, workload
-    from paper_2507_08523_amd.pipeline import (PagedPrefixCache, chunk_schedule, max_blocks_of,
+    from paper_2507_08523_amd.pipeline import (DecodeGraph, PagedPrefixCache, chunk_schedule, max_blocks_of,
                                                pool_blocks_needed, rope_inv_freq, shared_prefix_len)
 
     ilpc.load()
@@ -216,6 +220,9 @@ def main():
 
     if args.cascade and (args.rope or args.chunk_tokens):
         print("--cascade does not combine with --rope or --chunk-tokens", file=sys.stderr)
+        sys.exit(2)
+    if args.graph and (args.cascade or args.rope):
+        print("--graph does not combine with --cascade or --rope", file=sys.stderr)
         sys.exit(2)
     inv_freq = torch.from_numpy(rope_inv_freq(sp.head_dim, args.rope)).to(dev) if args.rope else None
 
@@ -260,6 +267,14 @@ def main():
     dec_out = [torch.empty_like(d["q"]) for d in dec_in]
     dec_rot = [torch.empty_like(d["q"]) for d in dec_in] if args.rope else None
     cu_dec = np.arange(len(L) + 1, dtype=np.int32)
+    dgraph = None
+    if args.graph and dec:
+        # the prefill's K/V must be in the pools before the eager pass of the capture
+        b = pc.upload_prefill(cached, tables, L, stream)
+        pc.append(b, k_new, v_new, stream)
+        torch.cuda.synchronize()
+        dgraph = DecodeGraph(pc, tables, L, dec_in, dec_out, sp.scale)
+        torch.cuda.synchronize()
     work = workload_work(wl, cached)
     n_tokens = work["query_tokens"] + dec * len(L)
 
@@ -291,7 +306,10 @@ def main():
             else:
                 pc.attend(b, q_rot if args.rope else q, out, sp.scale, stream)
         e[2].record(stream)
-        for s in range(dec):
+        if dgraph is not None:
+            assert np.array_equal(t, tables), "block tables changed since the capture"
+            dgraph.replay()
+        for s in range(dec if dgraph is None else 0):
             bd = pc.upload(t, cu_dec, L + s + 1, L + s, stream)
             qd = dec_in[s]["q"]
             if args.rope:
@@ -355,6 +373,7 @@ def main():
                    **({"cascade_shared_len": shared_len} if args.cascade else {}),
                    **({"chunk_tokens": args.chunk_tokens, "chunks": n_chunks} if args.chunk_tokens else {}),
                    **({"rope_base": args.rope} if args.rope else {}),
+                   **({"decode_graph": True} if dgraph is not None else {}),
                    **(icl or {})},
         "roofline": {**roof, **({"scope": f"all {n_chunks} chunked steps: appends, attention and the "
                                          "host's per-step metadata copies"} if args.chunk_tokens else {})},

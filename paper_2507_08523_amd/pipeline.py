@@ -226,6 +226,65 @@ class PagedPrefixCache:
         return ws
 
 
+class DecodeGraph:
+    """A run of decode steps captured once as a HIP graph and replayed as one launch.
+
+    Step s appends the new K/V row of every request at position L_r + s and
+    attends that request's one query row over keys 0 .. L_r + s.  The block
+    tables must already hold blocks for every decode position (a reserve at
+    match time).  All steps' metadata is staged, with one copy, into a device
+    buffer the graph owns; the per-step inputs (q, k_new, v_new: [B, H, D])
+    and outputs are the caller's tensors, read and written at every replay.
+    Replays repeat the same appends into the same slots, so they are
+    idempotent.  The capture stream keeps the default priority.
+    """
+
+    def __init__(self, pc: PagedPrefixCache, tables, seq_lens, inputs, outs, scale: float):
+        import torch
+
+        tables = np.ascontiguousarray(tables, dtype=np.int32)
+        B, mb = tables.shape
+        if mb != pc.max_blocks:
+            raise ilpc.ILPCError(ilpc.EINVAL, "DecodeGraph: block table width differs from max_blocks")
+        L = np.asarray(seq_lens, dtype=np.int32)
+        n = len(inputs)
+        per = B * mb + 3 * B + 1
+        host = np.empty(n * per, np.int32)
+        cu = np.arange(B + 1, dtype=np.int32)
+        for s in range(n):
+            o = s * per
+            host[o:o + B * mb] = tables.reshape(-1)
+            host[o + B * mb:o + B * mb + B + 1] = cu
+            host[o + B * mb + B + 1:o + B * mb + 2 * B + 1] = L + s + 1
+            host[o + B * mb + 2 * B + 1:o + per] = L + s
+        self.meta = torch.from_numpy(host).to(pc.device)
+        d = self.meta
+        self.batches = []
+        for s in range(n):
+            o = s * per
+            self.batches.append(DeviceBatch(block_tables=d[o:o + B * mb].view(B, mb),
+                                            cu_q=d[o + B * mb:o + B * mb + B + 1],
+                                            seq_lens=d[o + B * mb + B + 1:o + B * mb + 2 * B + 1],
+                                            start_pos=d[o + B * mb + 2 * B + 1:o + per],
+                                            max_q_len=1, total_q=B, B=B))
+        self.stream = torch.cuda.Stream(pc.device)
+        ilpc.attn_workspace(pc.device, self.stream)  # created (zero-filled) before the capture
+        self._run(pc, inputs, outs, scale)           # eager once on the capture stream
+        self.stream.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph, stream=self.stream):
+            self._run(pc, inputs, outs, scale)
+
+    def _run(self, pc, inputs, outs, scale):
+        for b, x, o in zip(self.batches, inputs, outs):
+            pc.append(b, x["k_new"], x["v_new"], self.stream)
+            pc.attend(b, x["q"], o, scale, self.stream)
+
+    def replay(self):
+        """Launch every captured step on the current stream."""
+        self.graph.replay()
+
+
 def chunk_schedule(q_lens, budget: int):
     """Scheduler steps of at most ``budget`` new tokens (max-num-batched-tokens).
 
