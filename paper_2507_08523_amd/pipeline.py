@@ -47,9 +47,12 @@ class PagedPrefixCache:
         self.k_pool, self.v_pool = ilpc.alloc_pools(num_blocks, n_kv_heads, head_dim, self.device)
         n = max_batch * max_blocks + 3 * max_batch + 1
         self._host = [torch.empty(n, dtype=torch.int32, pin_memory=True) for _ in range(2)]
-        self._host_ev = [None, None]
+        self._host_np = [h.numpy() for h in self._host]
+        self._host_ev = [torch.cuda.Event(), torch.cuda.Event()]
+        self._host_used = [False, False]
         self._flip = 0
         self._dev = torch.empty(n, dtype=torch.int32, device=self.device)
+        self._views = {}  # batch size -> device views of the metadata buffer
         self._steps_host = self._steps_dev = self._steps_ev = None
 
     # -- host ---------------------------------------------------------------
@@ -75,29 +78,34 @@ class PagedPrefixCache:
         B = int(tables.shape[0])
         if B > self.max_batch or tables.shape[1] != self.max_blocks:
             raise ilpc.ILPCError(ilpc.EINVAL, "upload: batch larger than the staging buffers")
-        stream = stream or torch.cuda.current_stream(self.device)
+        current = torch.cuda.current_stream(self.device)
+        stream = stream or current
         i = self._flip
         self._flip ^= 1
-        if self._host_ev[i] is not None:
+        if self._host_used[i]:
             self._host_ev[i].synchronize()  # the copy that last read this buffer is done
-        h = self._host[i]
+        h, hn = self._host[i], self._host_np[i]
         nbt = B * self.max_blocks
-        hn = h.numpy()
         hn[:nbt] = tables.reshape(-1)
         hn[nbt:nbt + B + 1] = cu_q
         hn[nbt + B + 1:nbt + 2 * B + 1] = seq_lens
         hn[nbt + 2 * B + 1:nbt + 3 * B + 1] = start_pos
         n = nbt + 3 * B + 1
-        with torch.cuda.stream(stream):
+        if stream == current:
             self._dev[:n].copy_(h[:n], non_blocking=True)
-            ev = torch.cuda.Event()
-            ev.record(stream)
-        self._host_ev[i] = ev
-        d = self._dev
+        else:
+            with torch.cuda.stream(stream):
+                self._dev[:n].copy_(h[:n], non_blocking=True)
+        self._host_ev[i].record(stream)
+        self._host_used[i] = True
+        views = self._views.get(B)
+        if views is None:
+            d = self._dev
+            views = (d[:nbt].view(B, self.max_blocks), d[nbt:nbt + B + 1], d[nbt + B + 1:nbt + 2 * B + 1],
+                     d[nbt + 2 * B + 1:nbt + 3 * B + 1])
+            self._views[B] = views
         q_lens = np.diff(np.asarray(cu_q, dtype=np.int64))
-        return DeviceBatch(block_tables=d[:nbt].view(B, self.max_blocks), cu_q=d[nbt:nbt + B + 1],
-                           seq_lens=d[nbt + B + 1:nbt + 2 * B + 1],
-                           start_pos=d[nbt + 2 * B + 1:nbt + 3 * B + 1],
+        return DeviceBatch(block_tables=views[0], cu_q=views[1], seq_lens=views[2], start_pos=views[3],
                            max_q_len=int(q_lens.max()) if B else 0, total_q=int(cu_q[-1]) if B else 0,
                            B=B)
 
