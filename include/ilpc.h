@@ -240,20 +240,50 @@ int ilpc_rope_kv_append(const uint16_t* q, uint16_t* q_out, int32_t Hq, const ui
  * Decode-shaped paged attention (section 2.1.2: each generated token attends
  * to the cached KV of its whole context): the same operation, arguments,
  * layouts and bounds rules as ilpc_paged_prefill_attn, for batches whose
- * max_q_len * (Hq / Hkv) <= 32 (ILPC_EUNSUP otherwise), with no workspace.
- * One wave per (request, kv head) streams that request's K/V blocks from the
- * pools; results agree with ilpc_paged_prefill_attn to the attention
- * tolerance, not bit for bit.  ilpc_paged_prefill_attn takes this path by
- * itself for such batches when B * Hkv >= the device's compute units.
+ * max_q_len * (Hq / Hkv) <= 32 (ILPC_EUNSUP otherwise).  One wave per
+ * (request, kv head) pair streams that request's K/V blocks from the pools;
+ * results agree with ilpc_paged_prefill_attn to the attention tolerance, not
+ * bit for bit.  ilpc_paged_prefill_attn takes this path by itself for such
+ * batches: split as ilpc_decode_split() says when its workspace has room for
+ * the partials, else unsplit when B * Hkv >= the device's compute units.
+ *
+ * n_split      [host] key ranges per pair, 1 .. 64, or 0 for
+ *                     ilpc_decode_split()'s choice.  With n > 1 each range is
+ *                     one wave; the ranges' partial results (fp32) go to the
+ *                     workspace and a second kernel merges them, so that
+ *                     batches with few pairs still occupy the whole chip.
+ * workspace    [device] >= ilpc_decode_workspace_bytes(..., n) bytes,
+ *                     16-byte aligned, no initial contents needed (NULL with
+ *                     0 bytes when n = 1).  Calls that may run concurrently
+ *                     need separate workspaces.
+ * A short or misaligned workspace, or n_split outside [0, 64], is ILPC_EINVAL.
  */
 int ilpc_paged_decode_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
                            int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
                            const int32_t* cu_q, const int32_t* seq_lens, int32_t B, int32_t max_q_len,
                            int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size, float softmax_scale,
-                           uint16_t* out, void* stream);
+                           uint16_t* out, int32_t n_split, void* workspace, size_t workspace_bytes,
+                           void* stream);
 
-/* Bytes of device workspace ilpc_paged_prefill_attn needs for these sizes
- * (currently 64 for every shape: the counters of its work queues). */
+/* The key-range count ilpc_paged_decode_attn uses for n_split = 0 on the
+ * current device: 1 when B * Hkv >= its SIMDs (4 per compute unit), and
+ * when B * Hkv >= half of them with a context bound 16 * max_blocks under
+ * 1024 tokens; otherwise enough ranges for one wave per SIMD, at most one
+ * per 32 keys of that bound, at most 64. */
+int ilpc_decode_split(int32_t B, int32_t Hkv, int32_t max_blocks, int32_t* n_split);
+
+/* Workspace bytes of ilpc_paged_decode_attn with n_split ranges:
+ * 0 for n_split = 1, else B * Hkv * n_split * min(32, max_q_len * Hq / Hkv) * (D + 2) * 4. */
+int ilpc_decode_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                                int32_t n_split, size_t* bytes);
+
+/* Bytes of device workspace ilpc_paged_prefill_attn needs for these sizes:
+ * 64 (the counters of its work queues), plus, for decode-shaped batches
+ * (max_q_len * Hq / Hkv <= 32) with fewer (request, kv head) pairs than the
+ * current device has SIMDs, room for the split decode kernel's partials
+ * (ilpc_decode_workspace_bytes() at the split of any context length).  A
+ * workspace of only 64 bytes is still accepted: such batches then run
+ * unsplit. */
 int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
                               size_t* bytes);
 
@@ -270,11 +300,13 @@ int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t 
  * max_q_len    [host]   >= every q_len_r; rows beyond it are not computed
  * softmax_scale         multiplies q.k before the softmax (1/sqrt(D) usually)
  * out          [device] bf16 [cu_q[B], Hq, D]
- * workspace    [device] >= ilpc_attn_workspace_bytes() bytes, 16-byte aligned,
- *                      zero-filled before its first use.  Each call leaves it
- *                      zero-filled again when its kernel completes, so calls
- *                      ordered on one stream can share it; calls that may run
- *                      concurrently (different streams) need separate ones.
+ * workspace    [device] >= 64 bytes (ilpc_attn_workspace_bytes() for every
+ *                      path), 16-byte aligned, its first 64 bytes zero-filled
+ *                      before the first use.  Each call leaves them zero-filled
+ *                      again when its kernels complete (the rest is scratch),
+ *                      so calls ordered on one stream can share it; calls that
+ *                      may run concurrently (different streams) need separate
+ *                      ones.
  *
  * Query t of request r sits at position L_r - q_len_r + t and attends to keys
  * 0 .. L_r - q_len_r + t; q head h reads kv head h / (Hq/Hkv).  Products and

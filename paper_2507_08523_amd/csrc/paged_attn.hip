@@ -25,6 +25,7 @@
 //    feeds the matrix core while the other computes the softmax.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <type_traits>
@@ -710,11 +711,42 @@ extern "C" int ilpc_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint
   return launch_status("ilpc_kv_append");
 }
 
+namespace {
+
+// Key ranges per (request, kv head) pair for the decode kernel.  With fewer
+// pairs than SIMDs on the chip: enough ranges for one wave per SIMD, at most
+// one per 32-key step of a 16 * max_blocks-token context (max_blocks = 0: no
+// such cap) and at most kMaxSplit.  Once the pairs give every SIMD pair a
+// wave, splitting pays only on contexts of at least kSplitLongSteps steps:
+// on shorter ones the merge launch costs more than the extra waves gain.
+constexpr int kSplitLongSteps = 32;
+
+int decode_auto_split(int64_t B, int64_t Hkv, int64_t max_blocks) {
+  const int64_t simds = int64_t(device_cus()) * 4;
+  const int64_t pairs = B * Hkv;
+  if (simds <= 0 || pairs <= 0 || pairs >= simds) return 1;
+  int64_t n = std::min<int64_t>((simds + pairs - 1) / pairs, ilpc::kMaxSplit);
+  if (max_blocks > 0) {
+    const int64_t steps = (max_blocks * kBlock + 31) / 32;
+    if (pairs * 2 >= simds && steps < kSplitLongSteps) return 1;
+    n = std::min(n, steps);
+  }
+  return int(n);
+}
+
+bool decode_shaped(int64_t max_q_len, int Hq, int Hkv) { return max_q_len * (Hq / Hkv) <= kDecodeCols; }
+
+}  // namespace
+
 extern "C" int ilpc_attn_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv,
                                          int32_t D, size_t* bytes) {
   if (!bytes || B < 0 || max_q_len < 0 || Hq < 1 || Hkv < 1 || D < 1)
     return ilpc::set_error(ILPC_EINVAL, "ilpc_attn_workspace_bytes: bad argument");
   *bytes = kQueueWords * sizeof(unsigned);
+  // room for the decode kernel's split partials (the largest split any
+  // context length can get) on decode-shaped batches with few pairs
+  if (B > 0 && max_q_len > 0 && decode_shaped(max_q_len, Hq, Hkv))
+    *bytes += ilpc::decode_split_bytes(B, max_q_len, Hq, Hkv, D, decode_auto_split(B, Hkv, 0));
   return ILPC_OK;
 }
 
@@ -795,11 +827,22 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
   if (!workspace || workspace_bytes < kQueueWords * sizeof(unsigned) || !aligned16(workspace))
     return ilpc::set_error(ILPC_EINVAL, "%s: workspace must be %zu bytes, 16-byte aligned", fn,
                            kQueueWords * sizeof(unsigned));
-  // Decode-shaped batches with enough (request, kv head) pairs to fill the
-  // chip go to the one-wave-per-pair kernel.
-  if (int64_t(max_q_len) * (Hq / Hkv) <= kDecodeCols && int64_t(B) * Hkv >= device_cus())
-    return ilpc::launch_decode_attn(q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
-                                    max_q_len, Hq, Hkv, D, softmax_scale * 1.4426950408889634f, out, stream);
+  // Decode-shaped batches go to the one-wave-per-pair kernel: split into key
+  // ranges when the pairs are fewer than the SIMDs and the workspace has room
+  // for the partials (after the queue counters), unsplit when the pairs at
+  // least fill the compute units.
+  if (decode_shaped(max_q_len, Hq, Hkv)) {
+    const float scale_log2 = softmax_scale * 1.4426950408889634f;
+    const int n_split = decode_auto_split(B, Hkv, max_blocks);
+    const size_t head = kQueueWords * sizeof(unsigned);
+    if (n_split > 1 && workspace_bytes >= head + ilpc::decode_split_bytes(B, max_q_len, Hq, Hkv, D, n_split))
+      return ilpc::launch_decode_attn(q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens,
+                                      B, max_q_len, Hq, Hkv, D, scale_log2, out, n_split,
+                                      reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + head), stream);
+    if (int64_t(B) * Hkv >= device_cus())
+      return ilpc::launch_decode_attn(q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens,
+                                      B, max_q_len, Hq, Hkv, D, scale_log2, out, 1, nullptr, stream);
+  }
   const int64_t col_tiles = (int64_t(max_q_len) * (Hq / Hkv) + kCols - 1) / kCols;
   return launch_attn<kFull>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
                             Hq, Hkv, D, col_tiles, softmax_scale * 1.4426950408889634f, out,
@@ -807,11 +850,29 @@ extern "C" int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool
                             static_cast<hipStream_t>(stream));
 }
 
+
+extern "C" int ilpc_decode_split(int32_t B, int32_t Hkv, int32_t max_blocks, int32_t* n_split) {
+  if (!n_split || B < 0 || Hkv < 1 || max_blocks < 1)
+    return ilpc::set_error(ILPC_EINVAL, "ilpc_decode_split: bad argument");
+  *n_split = decode_auto_split(B, Hkv, max_blocks);
+  return ILPC_OK;
+}
+
+extern "C" int ilpc_decode_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                                           int32_t n_split, size_t* bytes) {
+  if (!bytes || B < 0 || max_q_len < 0 || Hq < 1 || Hkv < 1 || D < 1 || n_split < 1 ||
+      n_split > ilpc::kMaxSplit)
+    return ilpc::set_error(ILPC_EINVAL, "ilpc_decode_workspace_bytes: bad argument");
+  *bytes = ilpc::decode_split_bytes(B, max_q_len, Hq, Hkv, D, n_split);
+  return ILPC_OK;
+}
+
 extern "C" int ilpc_paged_decode_attn(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
                                      int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
                                      const int32_t* cu_q, const int32_t* seq_lens, int32_t B, int32_t max_q_len,
                                      int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size,
-                                     float softmax_scale, uint16_t* out, void* stream) {
+                                     float softmax_scale, uint16_t* out, int32_t n_split, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
   static const char* fn = "ilpc_paged_decode_attn";
   int rc = check_attn_args(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
                            max_q_len, Hq, Hkv, D, block_size, softmax_scale, out);
@@ -819,8 +880,18 @@ extern "C" int ilpc_paged_decode_attn(const uint16_t* q, const uint16_t* k_pool,
   if (int64_t(max_q_len) * (Hq / Hkv) > kDecodeCols)
     return ilpc::set_error(ILPC_EUNSUP, "%s: max_q_len * Hq / Hkv = %lld > %d", fn,
                            (long long)max_q_len * (Hq / Hkv), kDecodeCols);
+  if (n_split < 0 || n_split > ilpc::kMaxSplit)
+    return ilpc::set_error(ILPC_EINVAL, "%s: n_split %d outside [0, %d]", fn, n_split, ilpc::kMaxSplit);
+  if (n_split == 0) n_split = decode_auto_split(B, Hkv, max_blocks);
+  if (int64_t(B) * Hkv * n_split > INT32_MAX)
+    return ilpc::set_error(ILPC_EUNSUP, "%s: B * Hkv * n_split too large", fn);
+  const size_t need = ilpc::decode_split_bytes(B, max_q_len, Hq, Hkv, D, n_split);
+  if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+    return ilpc::set_error(ILPC_EINVAL, "%s: %d key ranges need a %zu-byte workspace, 16-byte aligned", fn,
+                           n_split, need);
   return ilpc::launch_decode_attn(q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
-                                  max_q_len, Hq, Hkv, D, softmax_scale * 1.4426950408889634f, out, stream);
+                                  max_q_len, Hq, Hkv, D, softmax_scale * 1.4426950408889634f, out, n_split,
+                                  static_cast<float*>(workspace), stream);
 }
 
 extern "C" int ilpc_attn_cascade_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv,

@@ -42,7 +42,10 @@ _SIGS = [
     ("ilpc_paged_prefill_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
                                        _i32, _i32, _i32, _f32, _vp, _vp, ctypes.c_size_t, _vp]),
     ("ilpc_paged_decode_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
-                                      _i32, _i32, _i32, _f32, _vp, _vp]),
+                                      _i32, _i32, _i32, _f32, _vp, _i32, _vp, ctypes.c_size_t, _vp]),
+    ("ilpc_decode_split", _i32, [_i32, _i32, _i32, ctypes.POINTER(_i32)]),
+    ("ilpc_decode_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32, _i32,
+                                           ctypes.POINTER(ctypes.c_size_t)]),
     ("ilpc_attn_cascade_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32,
                                                  ctypes.POINTER(ctypes.c_size_t)]),
     ("ilpc_paged_prefill_attn_cascade", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32,
@@ -326,14 +329,19 @@ def attn_workspace_bytes(B, max_q_len, Hq, Hkv, D) -> int:
 
 
 _workspaces = {}
+_ws_bytes = {}
 
 
-def attn_workspace(device=None, stream=None):
-    """A zero-filled attention workspace kept for one (device, stream) pair.
+def attn_workspace(device=None, stream=None, nbytes: int = 64):
+    """An attention workspace of at least `nbytes` kept for one (device, stream)
+    pair, its first 64 bytes zero-filled.
 
-    The attention call leaves its workspace zero-filled again, so one buffer
-    serves every call issued on that stream; calls on different streams get
-    different buffers because concurrent calls must not share one.
+    The attention call leaves those bytes zero-filled again (the rest is
+    scratch), so one buffer serves every call issued on that stream; calls on
+    different streams get different buffers because concurrent calls must not
+    share one.  A request for more bytes than the kept buffer holds replaces
+    it with a larger one (an allocation: make the first call of a shape before
+    a graph capture).
     """
     import torch
 
@@ -341,8 +349,12 @@ def attn_workspace(device=None, stream=None):
         stream = torch.cuda.current_stream(device)
     key = (stream.device.index, stream.cuda_stream)
     ws = _workspaces.get(key)
-    if ws is None:
-        ws = torch.zeros(attn_workspace_bytes(0, 0, 1, 1, 1), dtype=torch.uint8, device=stream.device)
+    if ws is None or ws.numel() < nbytes:
+        if ws is not None:
+            ws.record_stream(stream)  # its memory is reused only after the stream's queued work
+        with torch.cuda.stream(stream):  # zero-filled in order with the calls that will use it
+            ws = torch.zeros(max(nbytes, attn_workspace_bytes(0, 0, 1, 1, 1)), dtype=torch.uint8,
+                             device=stream.device)
         _workspaces[key] = ws
     return ws
 
@@ -351,8 +363,10 @@ def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_le
                        out, workspace=None, stream=None):
     """Causal GQA attention of packed queries [total, Hq, D] over the paged pools.
 
-    `workspace` defaults to the zero-filled buffer attn_workspace() keeps for
-    the stream the call is issued on.
+    `workspace` defaults to the buffer attn_workspace() keeps for the stream
+    the call is issued on, grown to attn_workspace_bytes() for this shape
+    (decode-shaped batches with few (request, kv head) pairs use the room to
+    split each pair's keys over several waves).
     """
     import torch
 
@@ -364,7 +378,11 @@ def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_le
     if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
         raise ILPCError(EINVAL, "paged_prefill_attn: inconsistent batch shapes")
     if workspace is None:
-        workspace = attn_workspace(q.device, stream)
+        shape = (B, int(max_q_len), Hq, Hkv, D)
+        need = _ws_bytes.get(shape)
+        if need is None:
+            need = _ws_bytes[shape] = attn_workspace_bytes(*shape)
+        workspace = attn_workspace(q.device, stream, need)
     ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace", 1), workspace.numel()
     args = (_dev(q, torch.bfloat16, "q", 3), _dev(k_pool, torch.bfloat16, "k_pool", 4),
             _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
@@ -375,11 +393,30 @@ def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_le
     _check(load().ilpc_paged_prefill_attn(*args))
 
 
+def decode_split(B, Hkv, max_blocks) -> int:
+    """Key ranges per (request, kv head) the decode kernel uses by default."""
+    n = _i32()
+    _check(load().ilpc_decode_split(B, Hkv, max_blocks, ctypes.byref(n)))
+    return int(n.value)
+
+
+def decode_workspace_bytes(B, max_q_len, Hq, Hkv, D, n_split) -> int:
+    n = ctypes.c_size_t()
+    _check(load().ilpc_decode_workspace_bytes(B, max_q_len, Hq, Hkv, D, n_split, ctypes.byref(n)))
+    return int(n.value)
+
+
 def paged_decode_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_len: int, scale: float, out,
-                      stream=None):
+                      stream=None, n_split: int = 1, workspace=None):
     """The decode kernel alone (max_q_len * Hq / Hkv <= 32): same semantics as
-    paged_prefill_attn, which picks it by itself for such batches when they
-    have at least one (request, kv head) pair per compute unit."""
+    paged_prefill_attn, which picks it by itself (unsplit) for such batches
+    when they have at least one (request, kv head) pair per compute unit.
+
+    n_split > 1 cuts every pair's keys into that many ranges (0: the
+    library's choice, decode_split()); `workspace` is then a uint8 device
+    tensor of at least decode_workspace_bytes() bytes, allocated here when
+    omitted (an allocation: pass one in under graph capture).
+    """
     import torch
 
     NB, Hkv, bs, D = k_pool.shape
@@ -393,8 +430,15 @@ def paged_decode_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_len
             _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
             _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],
             _dev(cu_q, torch.int32, "cu_q", 1), _dev(seq_lens, torch.int32, "seq_lens", 1), B,
-            int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3), _stream(stream))
-    _check(load().ilpc_paged_decode_attn(*args))
+            int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3))
+    if n_split == 0:
+        n_split = decode_split(B, Hkv, block_tables.shape[1])
+    need = decode_workspace_bytes(B, int(max_q_len), Hq, Hkv, D, n_split) if n_split >= 1 else 0
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_ptr, ws_bytes = (None, 0) if workspace is None else (_dev(workspace, torch.uint8, "workspace", 1),
+                                                           workspace.numel())
+    _check(load().ilpc_paged_decode_attn(*args, int(n_split), ws_ptr, ws_bytes, _stream(stream)))
 
 
 def attn_cascade_workspace_bytes(B, max_q_len, Hq, Hkv, D) -> int:

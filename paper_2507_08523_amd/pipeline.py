@@ -276,7 +276,11 @@ class DecodeGraph:
                                             start_pos=d[o + B * mb + 2 * B + 1:o + per],
                                             max_q_len=1, total_q=B, B=B))
         self.stream = torch.cuda.Stream(pc.device)
-        ilpc.attn_workspace(pc.device, self.stream)  # created (zero-filled) before the capture
+        # the capture stream starts after the caller's queued work (appends, inputs)
+        self.stream.wait_stream(torch.cuda.current_stream(pc.device))
+        # the attention workspace is created before the capture
+        ilpc.attn_workspace(pc.device, self.stream,
+                            ilpc.attn_workspace_bytes(B, 1, inputs[0]["q"].shape[1], pc.n_kv_heads, pc.head_dim))
         self._run(pc, inputs, outs, scale)           # eager once on the capture stream
         self.stream.synchronize()
         self.graph = torch.cuda.CUDAGraph()

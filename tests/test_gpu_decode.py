@@ -1,8 +1,9 @@
 """GPU: the decode-shaped attention kernel (ilpc_paged_decode_attn) against the
 fp64 oracle, on every prompt of scaled workloads, with the last q_len tokens
 of each prompt as queries (q_len * Hq / Hkv up to 32), ragged lengths and
-physically permuted blocks; and the automatic choice of that kernel inside
-ilpc_paged_prefill_attn.
+physically permuted blocks, unsplit and with each pair's keys cut into
+several ranges (empty ranges and ranges where a query sees no key included);
+and the automatic choice of that kernel inside ilpc_paged_prefill_attn.
 """
 import sys
 
@@ -128,15 +129,52 @@ def test_decode_kernel_short_contexts_and_rejection():
 
 
 def test_prefill_entry_takes_the_decode_kernel_for_wide_batches():
-    # 64 prompts x 8 kv heads = 512 pairs >= 256 compute units: the automatic path
+    # 64 prompts x 8 kv heads = 512 pairs >= 256 compute units: the automatic
+    # path is the decode kernel, split as the library chooses when the
+    # workspace has room (fewer pairs than SIMDs), unsplit with 64 bytes
     f = Full(workload.scaled_spec("large", 64))
     sp = f.wl.spec
     q, cu, qn = f.queries(1)
-    out_auto, out_dec = torch.empty_like(q), torch.empty_like(q)
+    out_auto, out_dec, out_small, out_one = (torch.empty_like(q) for _ in range(4))
     b = f.pc.upload(f.tables, cu, f.wl.seq_lens, f.wl.seq_lens - qn)
     f.pc.attend(b, q, out_auto, sp.scale)
     ilpc.paged_decode_attn(q, f.pc.k_pool, f.pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, 1, sp.scale,
-                           out_dec)
+                           out_dec, n_split=0)
+    ilpc.paged_prefill_attn(q, f.pc.k_pool, f.pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, 1, sp.scale,
+                            out_small, torch.zeros(64, dtype=torch.uint8, device="cuda"))
+    ilpc.paged_decode_attn(q, f.pc.k_pool, f.pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, 1, sp.scale,
+                           out_one, n_split=1)
     torch.cuda.synchronize()
     assert torch.equal(out_auto, out_dec)
+    assert torch.equal(out_small, out_one)
     f.check(out_auto, cu, qn, "automatic")
+    f.check(out_small, cu, qn, "automatic, 64-byte workspace")
+
+
+def test_prefill_entry_splits_small_decode_batches():
+    # 6 prompts x 8 kv heads = 48 pairs: with a full-size workspace the entry
+    # runs the split decode kernel (the same bits as the library's split
+    # choice); with only the 64 queue bytes, the persistent kernel
+    f = Full(workload.scaled_spec("large", 6))
+    sp = f.wl.spec
+    q, cu, qn = f.queries(1)
+    b = f.pc.upload(f.tables, cu, f.wl.seq_lens, f.wl.seq_lens - qn)
+    B, mb = len(qn), b.block_tables.shape[1]
+    n = ilpc.decode_split(B, sp.n_kv_heads, mb)
+    assert n > 1
+    need = ilpc.attn_workspace_bytes(B, 1, sp.n_q_heads, sp.n_kv_heads, sp.head_dim)
+    assert need >= 64 + ilpc.decode_workspace_bytes(B, 1, sp.n_q_heads, sp.n_kv_heads, sp.head_dim, n)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    small = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    out_entry, out_split, out_small = (torch.empty_like(q) for _ in range(3))
+    ilpc.paged_prefill_attn(q, f.pc.k_pool, f.pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, 1, sp.scale,
+                            out_entry, ws)
+    ilpc.paged_decode_attn(q, f.pc.k_pool, f.pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, 1, sp.scale,
+                           out_split, n_split=0)
+    ilpc.paged_prefill_attn(q, f.pc.k_pool, f.pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, 1, sp.scale,
+                            out_small, small)
+    torch.cuda.synchronize()
+    assert torch.equal(out_entry, out_split)
+    assert int(ws[:64].count_nonzero()) == 0 and int(small.count_nonzero()) == 0
+    f.check(out_entry, cu, qn, f"prefill entry, {n} key ranges")
+    f.check(out_small, cu, qn, "prefill entry, 64-byte workspace")

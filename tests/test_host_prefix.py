@@ -219,3 +219,13 @@ def test_cascade_workspace_bytes_host_only():
     assert ilpc.attn_cascade_workspace_bytes(8, 100, Hq, 8, D) == 256 + o_bytes + ml_bytes
     with pytest.raises(ilpc.ILPCError):
         ilpc.attn_cascade_workspace_bytes(-1, 0, 1, 1, 64)
+
+
+def test_decode_workspace_bytes_formula():
+    # B * Hkv * n_split * min(32, max_q_len * G) * (D + 2) fp32 values; none unsplit
+    assert ilpc.decode_workspace_bytes(4, 1, 64, 8, 128, 16) == 4 * 8 * 16 * 8 * 130 * 4
+    assert ilpc.decode_workspace_bytes(3, 8, 28, 4, 128, 5) == 3 * 4 * 5 * 32 * 130 * 4  # 56 columns -> 32
+    assert ilpc.decode_workspace_bytes(7, 2, 4, 1, 64, 1) == 0
+    for bad in ((4, 1, 64, 8, 128, 0), (4, 1, 64, 8, 128, 65), (-1, 1, 64, 8, 128, 2)):
+        with pytest.raises(ilpc.ILPCError):
+            ilpc.decode_workspace_bytes(*bad)
