@@ -18,7 +18,7 @@ dominant kernel, the prefill attention launch, timed with HIP events on the
 stream it runs on.  ``cpu_baseline`` times the fp64 oracle on a bounded
 sample of the same workload on the host cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--cascade] [--no-pair]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--prompts N] [--cascade] [--no-pair]
 
 ``--cascade`` runs the prefill attention split at the prefix every prompt of
 the batch shares (ilpc_paged_prefill_attn_cascade).
@@ -29,7 +29,9 @@ append (ilpc_rope_kv_append; the warm prefix is rotated the same way).
 tokens (append + attention per step); the attention timing and ``roofline``
 then cover all steps.  ``--graph`` (decode workloads) captures the 32 decode
 steps once as a HIP graph with all their metadata on the device, and every
-timed step replays it.
+timed step replays it.  ``--prompts N`` keeps the workload's shapes with N
+prompts (``large --prompts 16``: decode steps of a small batch, whose
+attention splits each request's keys over several waves).
 
 ICL stream workloads (``icl_llama8b``): 2000 log-parsing requests whose
 demonstrations a selector picks with hot templates.  Before the timed steps the
@@ -169,6 +171,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama8b")
+    ap.add_argument("--prompts", type=int, default=0,
+                    help="run the workload's shapes with this many prompts (0: its own count)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle attention to time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-pair", action="store_true",
@@ -210,7 +214,12 @@ def main():
 
     icl = None
     if workload.SPECS[args.workload].n_templates:
+        if args.prompts:
+            print("--prompts does not apply to ICL stream workloads", file=sys.stderr)
+            sys.exit(2)
         icl, wl = icl_stream_workload(args.workload, not args.no_pair)
+    elif args.prompts:
+        wl = workload.build(workload.scaled_spec(args.workload, args.prompts))
     else:
         wl = workload.build(args.workload)
     wl.materialize(dev)
@@ -345,7 +354,7 @@ def main():
     # the prefill launch is bound by whichever roofline limit is higher for it
     t_mfma = work["flops"] / (PEAK_BF16_TFLOPS * 1e12)
     t_hbm = work["logical_bytes"] / (PEAK_HBM_GBS * 1e9)
-    traffic = traffic_from_profile(args.workload)
+    traffic = None if args.prompts else traffic_from_profile(args.workload)
     if t_mfma >= t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic}
