@@ -51,8 +51,10 @@ class PagedPrefixCache:
         self._host_ev = [torch.cuda.Event(), torch.cuda.Event()]
         self._host_used = [False, False]
         self._flip = 0
-        self._dev = torch.empty(n, dtype=torch.int32, device=self.device)
-        self._views = {}  # batch size -> device views of the metadata buffer
+        # Host and device staging are both double-buffered: the DeviceBatch of
+        # an upload stays valid until the second upload after it.
+        self._dev = [torch.empty(n, dtype=torch.int32, device=self.device) for _ in range(2)]
+        self._views = {}  # (buffer, batch size) -> device views of that metadata buffer
         self._steps_host = self._steps_dev = self._steps_ev = None
 
     # -- host ---------------------------------------------------------------
@@ -72,7 +74,13 @@ class PagedPrefixCache:
     # -- host -> device -----------------------------------------------------
     def upload(self, tables: np.ndarray, cu_q: np.ndarray, seq_lens: np.ndarray,
                start_pos: np.ndarray, stream=None) -> DeviceBatch:
-        """Stage metadata in pinned memory and copy it with one async H2D copy."""
+        """Stage metadata in pinned memory and copy it with one async H2D copy.
+
+        The returned views stay valid until the second upload after this one
+        (the staging buffers alternate).  The copy is queued on ``stream``;
+        work that reads the views must be ordered after it (same stream, or an
+        event the caller waits on) and before that later upload's copy.
+        """
         import torch
 
         B = int(tables.shape[0])
@@ -91,19 +99,19 @@ class PagedPrefixCache:
         hn[nbt + B + 1:nbt + 2 * B + 1] = seq_lens
         hn[nbt + 2 * B + 1:nbt + 3 * B + 1] = start_pos
         n = nbt + 3 * B + 1
+        dev = self._dev[i]
         if stream == current:
-            self._dev[:n].copy_(h[:n], non_blocking=True)
+            dev[:n].copy_(h[:n], non_blocking=True)
         else:
             with torch.cuda.stream(stream):
-                self._dev[:n].copy_(h[:n], non_blocking=True)
+                dev[:n].copy_(h[:n], non_blocking=True)
         self._host_ev[i].record(stream)
         self._host_used[i] = True
-        views = self._views.get(B)
+        views = self._views.get((i, B))
         if views is None:
-            d = self._dev
-            views = (d[:nbt].view(B, self.max_blocks), d[nbt:nbt + B + 1], d[nbt + B + 1:nbt + 2 * B + 1],
-                     d[nbt + 2 * B + 1:nbt + 3 * B + 1])
-            self._views[B] = views
+            views = (dev[:nbt].view(B, self.max_blocks), dev[nbt:nbt + B + 1], dev[nbt + B + 1:nbt + 2 * B + 1],
+                     dev[nbt + 2 * B + 1:nbt + 3 * B + 1])
+            self._views[(i, B)] = views
         q_lens = np.diff(np.asarray(cu_q, dtype=np.int64))
         return DeviceBatch(block_tables=views[0], cu_q=views[1], seq_lens=views[2], start_pos=views[3],
                            max_q_len=int(q_lens.max()) if B else 0, total_q=int(cu_q[-1]) if B else 0,
@@ -114,7 +122,8 @@ class PagedPrefixCache:
         staged together and sent with one async H2D copy; returns a DeviceBatch each.
 
         The staging buffers grow on demand (a first call may allocate) and are
-        reused: a later call first waits for the copy that last read them.
+        reused: a later call first waits for the copy that last read them, and
+        the batches it returned are valid only until that later call.
         """
         import torch
 

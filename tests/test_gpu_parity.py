@@ -244,6 +244,18 @@ def test_physical_block_permutation_and_rerun_bit_identical():
     assert torch.equal(a.attend(), first)
 
 
+def test_upload_views_survive_the_next_upload():
+    """The metadata staging alternates between two buffers, so a batch's views
+    stay valid across the next upload (here: other prompts' metadata)."""
+    run = Run("tiny")
+    first = run.out.clone()
+    # the same tables as a full prefill: other query offsets and start positions
+    b2 = run.pc.upload_prefill(np.zeros_like(run.cached), run.tables, run.wl.seq_lens)
+    torch.cuda.synchronize()
+    assert not torch.equal(b2.cu_q, run.batch.cu_q)
+    assert torch.equal(run.attend(), first)
+
+
 def test_fully_cached_prompt_and_ragged_group():
     # L % 16 == 0 and already registered: S = 16 recomputed; G = 7 columns
     spec = workload.WorkloadSpec(name="capcase", n_q_heads=28, n_kv_heads=4, head_dim=128, n_prompts=3,
