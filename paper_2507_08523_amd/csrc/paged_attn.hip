@@ -93,14 +93,6 @@ __device__ __forceinline__ void global_to_lds16(const void* src, uint8_t* lds) {
 }
 #pragma clang diagnostic pop
 
-// max of three floats in one instruction (v_max3_f32; the operands come from
-// the matrix cores or are -inf, never signalling NaNs, so no quieting is needed)
-__device__ __forceinline__ float max3f(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
-
 // max(x, x of the lane 32 apart): v_permlane32_swap exchanges the two wave halves.
 __device__ __forceinline__ float max_across_halves(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -369,7 +361,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     auto usable = [&](int tl, int id) {
       return ((t0 + tl) * kTileBlocks + my_blk < n_blk_used && id >= 0 && id < num_blocks) ? id : 0;
     };
-    auto stage = [&](int tl) { return ring + ((tbase + tl) % kStages) * kStageBytes; };
+    auto stage = [&](int tl) { return ring + (unsigned(tbase + tl) % unsigned(kStages)) * kStageBytes; };
     auto issue_tile = [&](int tl, int raw) {
       const int id = usable(tl, raw);
       uint8_t* st = stage(tl);
@@ -456,11 +448,37 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
           sc1[e] = k + 32 < lo ? -INFINITY : sc1[e];
         }
       }
-      float mx = max3f(sc0[0], sc1[0], sc0[1]);
-      mx = max3f(mx, sc1[1], sc0[2]);
-#pragma unroll
-      for (int e = 2; e < 15; ++e) mx = max3f(mx, sc1[e], sc0[e + 1]);
-      mx = max3f(mx, sc1[15], mx);
+      // Column max: 16 dependent v_max3_f32 in two asm statements (the
+      // operands come from the matrix cores or are -inf, never signalling
+      // NaNs, so no quieting is needed).  The compiler follows every
+      // inline-asm statement with a wait state, so one statement per
+      // instruction would add 16 of them to the chain.
+      float mx, mx2;
+      asm("v_max3_f32 %0, %1, %2, %3\n\t"
+          "v_max3_f32 %0, %0, %4, %5\n\t"
+          "v_max3_f32 %0, %0, %6, %7\n\t"
+          "v_max3_f32 %0, %0, %8, %9\n\t"
+          "v_max3_f32 %0, %0, %10, %11\n\t"
+          "v_max3_f32 %0, %0, %12, %13\n\t"
+          "v_max3_f32 %0, %0, %14, %15\n\t"
+          "v_max3_f32 %0, %0, %16, %17"
+          : "=&v"(mx)
+          : "v"(sc0[0]), "v"(sc1[0]), "v"(sc0[1]), "v"(sc1[1]), "v"(sc0[2]), "v"(sc1[2]), "v"(sc0[3]),
+            "v"(sc1[3]), "v"(sc0[4]), "v"(sc1[4]), "v"(sc0[5]), "v"(sc1[5]), "v"(sc0[6]), "v"(sc1[6]),
+            "v"(sc0[7]), "v"(sc1[7]), "v"(sc0[8]));
+      asm("v_max3_f32 %0, %1, %2, %3\n\t"
+          "v_max3_f32 %0, %0, %4, %5\n\t"
+          "v_max3_f32 %0, %0, %6, %7\n\t"
+          "v_max3_f32 %0, %0, %8, %9\n\t"
+          "v_max3_f32 %0, %0, %10, %11\n\t"
+          "v_max3_f32 %0, %0, %12, %13\n\t"
+          "v_max3_f32 %0, %0, %14, %15\n\t"
+          "v_max3_f32 %0, %0, %16, %0"
+          : "=&v"(mx2)
+          : "v"(mx), "v"(sc1[8]), "v"(sc0[9]), "v"(sc1[9]), "v"(sc0[10]), "v"(sc1[10]), "v"(sc0[11]),
+            "v"(sc1[11]), "v"(sc0[12]), "v"(sc1[12]), "v"(sc0[13]), "v"(sc1[13]), "v"(sc0[14]),
+            "v"(sc1[14]), "v"(sc0[15]), "v"(sc1[15]));
+      mx = mx2;
       mx = max_across_halves(mx) * scale_log2;
       if (__ballot(mx > m_used + kLazyRescale)) {
         const float m_new = fmaxf(m_used, mx);
