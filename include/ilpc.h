@@ -375,7 +375,9 @@ int ilpc_paged_prefill_attn_cascade(const uint16_t* q, const uint16_t* k_pool, c
 typedef struct ilpc_pair_table ilpc_pair_table; /* opaque, host memory, library-owned */
 
 /* Create an empty ICL table holding at most `capacity` sets (1 .. 2^24) of
- * `n_demos` demonstrations (1 .. 4096).  *out receives the handle. */
+ * `n_demos` demonstrations (1 .. 4096).  *out receives the handle (NULL on
+ * error).  All of the table's memory is taken here: ILPC_ENOSPC if the host
+ * cannot provide it, ILPC_EINVAL for sizes out of range. */
 int ilpc_pair_create(int32_t capacity, int32_t n_demos, ilpc_pair_table** out);
 
 /* Free a table (NULL is ignored). */
@@ -404,8 +406,10 @@ int ilpc_pair_reset(ilpc_pair_table* table);
  * recently used; PMC = 0 appends the current set unchanged; otherwise the
  * final set is appended and the target keeps its place.  A set already held
  * is stored once (appending it refreshes it); beyond the capacity the least
- * recently used set is evicted.  On error the table is unchanged only if the
- * error is reported before the first request (NULL pointer, negative B).
+ * recently used set is evicted.  Errors (NULL table or pointer, negative B:
+ * ILPC_EINVAL) are reported before anything changes; otherwise the call
+ * completes, since every structure the table uses was sized by
+ * ilpc_pair_create and refinement allocates nothing.
  */
 int ilpc_pair_refine(ilpc_pair_table* table, const int32_t* templates, const int32_t* demos, int32_t B,
                      int32_t* out_templates, int32_t* out_demos, int32_t* pmc);

@@ -415,8 +415,8 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     f32x16 sc0, sc1;           // scores of the tile whose softmax is next
 
     // Softmax step of the score tile starting at key j0: causal mask, column
-    // max, lazy rescale of O, P = exp2(S * scale_log2 - m) as bf16 (the sum
-    // uses the same bf16 values).
+    // max, lazy rescale of O, P = exp2(S * scale_log2 - m), rounded to bf16
+    // for the V^T P^T product while the row sum adds the fp32 values.
     // Lane half hh holds keys j0 + (e>>3)*16 + 8*hh + (e&7) [+32] of the tile.
     auto softmax = [&](int j0) {
       if (MODE != kShared && j0 + kKeys - 1 > wave_pos_min) {  // causal

@@ -24,10 +24,15 @@
 // Only past sets whose first template occurs in the current set can have a
 // PMC above 0, so the table keeps an index from first template to sets, and a
 // request looks at those sets only.
+//
+// Every structure the table uses (the slot arrays, both hash indexes and the
+// per-request scratch) is sized when the table is created, so refinement
+// allocates nothing: a call either is refused before it changes anything or
+// completes.
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <new>
-#include <unordered_map>
 #include <vector>
 
 #include "../../include/ilpc.h"
@@ -54,6 +59,39 @@ uint64_t set_key(const int32_t* tmpl, const int32_t* demo, int32_t n) {
   return h;
 }
 
+// A hash index over the table's slots: buckets of doubly linked slot chains,
+// all arrays sized for the capacity at creation.
+struct SlotIndex {
+  uint64_t mask = 0;
+  std::vector<int32_t> bucket, nxt, prv;  // bucket heads; per-slot chain links (-1: none)
+
+  void init(int32_t cap) {
+    uint64_t nb = 1;
+    while (nb < 2 * uint64_t(cap)) nb <<= 1;
+    mask = nb - 1;
+    bucket.assign(size_t(nb), -1);
+    nxt.assign(size_t(cap), -1);
+    prv.assign(size_t(cap), -1);
+  }
+  void clear() { std::fill(bucket.begin(), bucket.end(), -1); }
+  int32_t head(uint64_t h) const { return bucket[size_t(h & mask)]; }
+  void insert(uint64_t h, int32_t s) {
+    int32_t& b = bucket[size_t(h & mask)];
+    prv[s] = -1;
+    nxt[s] = b;
+    if (b >= 0) prv[b] = s;
+    b = s;
+  }
+  void erase(uint64_t h, int32_t s) {
+    if (prv[s] >= 0) nxt[prv[s]] = nxt[s];
+    else bucket[size_t(h & mask)] = nxt[s];
+    if (nxt[s] >= 0) prv[nxt[s]] = prv[s];
+    prv[s] = nxt[s] = -1;
+  }
+};
+
+inline uint64_t first_hash(int32_t t) { return mix64(uint64_t(uint32_t(t)) ^ 0x3C6EF372FE94F82Bull); }
+
 }  // namespace
 
 struct ilpc_pair_table {
@@ -65,8 +103,11 @@ struct ilpc_pair_table {
   std::vector<uint8_t> live;
   int32_t head = -1, tail = -1, size = 0, free_head = -1;
   uint64_t clock = 0;
-  std::unordered_map<uint64_t, std::vector<int32_t>> by_key;    // set key -> slots
-  std::unordered_map<int32_t, std::vector<int32_t>> by_first;   // first template -> slots
+  SlotIndex by_key;    // set key -> slots (contents compared on a hit)
+  SlotIndex by_first;  // first template -> slots (first template compared on a hit)
+  // Per-request scratch: distinct templates of the current set and their
+  // counts, the counts left while matching, replaced flags, the final set.
+  std::vector<int32_t> w_tk, w_tc, w_avail, w_used, w_ft, w_fd;
 
   void init(int32_t cap, int32_t n_demos) {
     capacity = cap;
@@ -78,6 +119,9 @@ struct ilpc_pair_table {
     stamp.assign(cap, 0);
     key.assign(cap, 0);
     live.assign(cap, 0);
+    by_key.init(cap);
+    by_first.init(cap);
+    for (auto* v : {&w_tk, &w_tc, &w_avail, &w_used, &w_ft, &w_fd}) v->assign(size_t(n), 0);
     clear();
   }
   void clear() {
@@ -89,14 +133,6 @@ struct ilpc_pair_table {
     std::fill(live.begin(), live.end(), 0);
     free_head = capacity > 0 ? 0 : -1;
     for (int32_t s = 0; s < capacity; ++s) next[s] = s + 1 < capacity ? s + 1 : -1;
-  }
-  static void erase_from(std::vector<int32_t>& v, int32_t s) {
-    for (size_t i = 0; i < v.size(); ++i)
-      if (v[i] == s) {
-        v[i] = v.back();
-        v.pop_back();
-        return;
-      }
   }
   void unlink(int32_t s) {
     if (prev[s] >= 0) next[prev[s]] = next[s];
@@ -120,22 +156,16 @@ struct ilpc_pair_table {
   void evict_head() {
     const int32_t s = head;
     unlink(s);
-    auto it = by_key.find(key[s]);
-    erase_from(it->second, s);
-    if (it->second.empty()) by_key.erase(it);
-    auto jt = by_first.find(tmpl[size_t(s) * n]);
-    erase_from(jt->second, s);
-    if (jt->second.empty()) by_first.erase(jt);
+    by_key.erase(key[s], s);
+    by_first.erase(first_hash(tmpl[size_t(s) * n]), s);
     live[s] = 0;
     next[s] = free_head;
     free_head = s;
     --size;
   }
   int32_t find(const int32_t* t, const int32_t* d, uint64_t k) const {
-    auto it = by_key.find(k);
-    if (it == by_key.end()) return -1;
-    for (int32_t s : it->second)
-      if (!memcmp(&tmpl[size_t(s) * n], t, sizeof(int32_t) * n) &&
+    for (int32_t s = by_key.head(k); s >= 0; s = by_key.nxt[s])
+      if (key[s] == k && !memcmp(&tmpl[size_t(s) * n], t, sizeof(int32_t) * n) &&
           !memcmp(&demo[size_t(s) * n], d, sizeof(int32_t) * n))
         return s;
     return -1;
@@ -157,8 +187,8 @@ struct ilpc_pair_table {
     key[s] = k;
     live[s] = 1;
     link_tail(s);
-    by_key[k].push_back(s);
-    by_first[t[0]].push_back(s);
+    by_key.insert(k, s);
+    by_first.insert(first_hash(t[0]), s);
     ++size;
   }
 };
@@ -172,12 +202,12 @@ extern "C" int ilpc_pair_create(int32_t capacity, int32_t n_demos, ilpc_pair_tab
   if (n_demos < 1 || n_demos > kMaxDemos)
     return set_error(ILPC_EINVAL, "ilpc_pair_create: n_demos %d outside [1, %d]", n_demos, kMaxDemos);
   ilpc_pair_table* t = new (std::nothrow) ilpc_pair_table();
-  if (!t) return set_error(ILPC_EINVAL, "ilpc_pair_create: out of host memory");
+  if (!t) return set_error(ILPC_ENOSPC, "ilpc_pair_create: out of host memory");
   try {
     t->init(capacity, n_demos);
   } catch (...) {
     delete t;
-    return set_error(ILPC_EINVAL, "ilpc_pair_create: out of host memory");
+    return set_error(ILPC_ENOSPC, "ilpc_pair_create: out of host memory");
   }
   *out = t;
   return ILPC_OK;
@@ -201,83 +231,78 @@ extern "C" int ilpc_pair_refine(ilpc_pair_table* table, const int32_t* templates
     return set_error(ILPC_EINVAL, "ilpc_pair_refine: NULL pointer");
   ilpc_pair_table& T = *table;
   const int32_t n = T.n;
-  try {
-    // distinct templates of the current set with their multiplicities
-    std::vector<int32_t> tk, tc, avail, used(n);
-    std::vector<int32_t> final_t(n), final_d(n);
-    for (int32_t b = 0; b < B; ++b) {
-      const int32_t* ct = templates + size_t(b) * n;
-      const int32_t* cd = demos + size_t(b) * n;
-      tk.clear();
-      tc.clear();
-      for (int32_t i = 0; i < n; ++i) {
-        size_t j = 0;
-        while (j < tk.size() && tk[j] != ct[i]) ++j;
-        if (j == tk.size()) {
-          tk.push_back(ct[i]);
-          tc.push_back(0);
-        }
-        ++tc[j];
+  int32_t* tk = T.w_tk.data();  // distinct templates of the current set
+  int32_t* tc = T.w_tc.data();  // their multiplicities
+  int32_t* avail = T.w_avail.data();
+  int32_t* used = T.w_used.data();
+  int32_t* final_t = T.w_ft.data();
+  int32_t* final_d = T.w_fd.data();
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t* ct = templates + size_t(b) * n;
+    const int32_t* cd = demos + size_t(b) * n;
+    int32_t nt = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      int32_t j = 0;
+      while (j < nt && tk[j] != ct[i]) ++j;
+      if (j == nt) {
+        tk[nt] = ct[i];
+        tc[nt++] = 0;
       }
-      // matching: candidates are the sets starting with a template of the current set
-      int32_t best = -1, best_k = 0;
-      for (size_t u = 0; u < tk.size(); ++u) {
-        auto it = T.by_first.find(tk[u]);
-        if (it == T.by_first.end()) continue;
-        for (int32_t s : it->second) {
-          avail = tc;
-          const int32_t* ht = &T.tmpl[size_t(s) * n];
-          int32_t k = 0;
-          for (; k < n; ++k) {
-            size_t j = 0;
-            while (j < tk.size() && tk[j] != ht[k]) ++j;
-            if (j == tk.size() || avail[j] == 0) break;
-            --avail[j];
-          }
-          if (k > best_k || (k == best_k && k > 0 && T.stamp[s] > T.stamp[best])) {
-            best = s;
-            best_k = k;
-          }
-        }
-      }
-      int32_t* ot = out_templates + size_t(b) * n;
-      int32_t* od = out_demos + size_t(b) * n;
-      if (best_k == n) {  // rule (1): the target set as it is, refreshed
-        memcpy(final_t.data(), &T.tmpl[size_t(best) * n], sizeof(int32_t) * n);
-        memcpy(final_d.data(), &T.demo[size_t(best) * n], sizeof(int32_t) * n);
-        T.touch(best);
-      } else if (best_k == 0) {  // rule (2): unchanged, appended
-        memcpy(final_t.data(), ct, sizeof(int32_t) * n);
-        memcpy(final_d.data(), cd, sizeof(int32_t) * n);
-        T.append(final_t.data(), final_d.data());
-      } else {  // rule (3): modified and reordered, appended
-        std::fill(used.begin(), used.end(), 0);
-        const int32_t* ht = &T.tmpl[size_t(best) * n];
-        const int32_t* hd = &T.demo[size_t(best) * n];
-        for (int32_t k = 0; k < best_k; ++k) {
-          for (int32_t i = 0; i < n; ++i)
-            if (!used[i] && ct[i] == ht[k]) {
-              used[i] = 1;
-              break;
-            }
-          final_t[k] = ht[k];
-          final_d[k] = hd[k];
-        }
-        int32_t m = best_k;
-        for (int32_t i = 0; i < n; ++i)
-          if (!used[i]) {
-            final_t[m] = ct[i];
-            final_d[m] = cd[i];
-            ++m;
-          }
-        T.append(final_t.data(), final_d.data());
-      }
-      memcpy(ot, final_t.data(), sizeof(int32_t) * n);
-      memcpy(od, final_d.data(), sizeof(int32_t) * n);
-      pmc[b] = best_k;
+      ++tc[j];
     }
-  } catch (...) {
-    return set_error(ILPC_EINVAL, "ilpc_pair_refine: out of host memory");
+    // matching: candidates are the sets starting with a template of the current set
+    int32_t best = -1, best_k = 0;
+    for (int32_t u = 0; u < nt; ++u) {
+      for (int32_t s = T.by_first.head(first_hash(tk[u])); s >= 0; s = T.by_first.nxt[s]) {
+        const int32_t* ht = &T.tmpl[size_t(s) * n];
+        if (ht[0] != tk[u]) continue;  // another template in the same bucket
+        std::copy(tc, tc + nt, avail);
+        int32_t k = 0;
+        for (; k < n; ++k) {
+          int32_t j = 0;
+          while (j < nt && tk[j] != ht[k]) ++j;
+          if (j == nt || avail[j] == 0) break;
+          --avail[j];
+        }
+        if (k > best_k || (k == best_k && k > 0 && T.stamp[s] > T.stamp[best])) {
+          best = s;
+          best_k = k;
+        }
+      }
+    }
+    if (best_k == n) {  // rule (1): the target set as it is, refreshed
+      memcpy(final_t, &T.tmpl[size_t(best) * n], sizeof(int32_t) * n);
+      memcpy(final_d, &T.demo[size_t(best) * n], sizeof(int32_t) * n);
+      T.touch(best);
+    } else if (best_k == 0) {  // rule (2): unchanged, appended
+      memcpy(final_t, ct, sizeof(int32_t) * n);
+      memcpy(final_d, cd, sizeof(int32_t) * n);
+      T.append(final_t, final_d);
+    } else {  // rule (3): modified and reordered, appended
+      std::fill(used, used + n, 0);
+      const int32_t* ht = &T.tmpl[size_t(best) * n];
+      const int32_t* hd = &T.demo[size_t(best) * n];
+      for (int32_t k = 0; k < best_k; ++k) {
+        for (int32_t i = 0; i < n; ++i)
+          if (!used[i] && ct[i] == ht[k]) {
+            used[i] = 1;
+            break;
+          }
+        final_t[k] = ht[k];
+        final_d[k] = hd[k];
+      }
+      int32_t m = best_k;
+      for (int32_t i = 0; i < n; ++i)
+        if (!used[i]) {
+          final_t[m] = ct[i];
+          final_d[m] = cd[i];
+          ++m;
+        }
+      T.append(final_t, final_d);
+    }
+    memcpy(out_templates + size_t(b) * n, final_t, sizeof(int32_t) * n);
+    memcpy(out_demos + size_t(b) * n, final_d, sizeof(int32_t) * n);
+    pmc[b] = best_k;
   }
   return ILPC_OK;
 }

@@ -26,16 +26,16 @@
 namespace ilpc {
 
 namespace {
-thread_local std::string g_last_error;
+// A fixed buffer: recording an error allocates nothing, so it also works
+// when the error is running out of memory.
+thread_local char g_last_error[512];
 }
 
 int set_error(int code, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return code;
 }
 
@@ -174,7 +174,7 @@ struct ilpc_cache {
 
 using ilpc::set_error;
 
-extern "C" const char* ilpc_last_error(void) { return ilpc::g_last_error.c_str(); }
+extern "C" const char* ilpc_last_error(void) { return ilpc::g_last_error; }
 
 namespace {
 
@@ -316,17 +316,24 @@ extern "C" int ilpc_prefix_match(ilpc_cache* cache, const int32_t* tokens,
   }
 
   // Keys of every full block, and the matched run of each request (read-only pass).
+  // Every allocation of the call happens here, before any state changes
+  // (the bump cache's registration journal is grown to hold this batch's
+  // keys too), so a call that runs out of host memory changes nothing.
   std::vector<uint64_t> keys;
-  std::vector<int64_t> key_off(static_cast<size_t>(B) + 1);
-  std::vector<int32_t> matched(static_cast<size_t>(B));
-  std::vector<int32_t> hit_ids;
+  std::vector<int64_t> key_off, hit_off;
+  std::vector<int32_t> matched, hit_ids;
   try {
     keys.resize(size_t(total_keys));
+    key_off.resize(size_t(B) + 1);
+    hit_off.resize(size_t(B) + 1);
+    matched.resize(size_t(B));
     hit_ids.reserve(size_t(total_keys));
+    const size_t jneed = cache->journal.size() + size_t(total_keys);
+    if (reg && !cache->lru && jneed > cache->journal.capacity())
+      cache->journal.reserve(std::max(jneed, 2 * cache->journal.capacity()));
   } catch (...) {
     return set_error(ILPC_ENOSPC, "ilpc_prefix_match: out of host memory");
   }
-  std::vector<int64_t> hit_off(static_cast<size_t>(B) + 1);
   int64_t ko = 0;
   for (int32_t r = 0; r < B; ++r) {
     const int32_t* t = tokens + cu_seqlens[r];
