@@ -18,7 +18,17 @@ dominant kernel, the prefill attention launch, timed with HIP events on the
 stream it runs on.  ``cpu_baseline`` times the fp64 oracle on a bounded
 sample of the same workload on the host cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--prompts N] [--cascade] [--no-pair]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload large] [--prompts N] [--cascade] [--no-pair]
+
+The default workload is ``large``: 512 prompts of 2112 tokens (16 demonstrations
+of 128 tokens + a 64-token query; 64 q / 8 kv heads, head_dim 128), whose
+prefill is followed by 32 decode steps -- the largest configuration that fits
+one GPU.  The roofline of the prefill launch is
+t_roof = max(FLOPs / 2.5 PFLOP/s, unique bytes / 8 TB/s), unique bytes
+counting each physical K/V block once; logical bytes (K/V once per request)
+are reported beside them.  ``--flush-mib N`` writes N MiB of device memory
+before every step, so HBM-bound launches do not find the previous step's data
+in the caches.
 
 ``--cascade`` runs the prefill attention split at the prefix every prompt of
 the batch shares (ilpc_paged_prefill_attn_cascade).
@@ -47,6 +57,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -62,18 +73,33 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak
 KERNEL_SRC = os.path.join(ROOT, "paper_2507_08523_amd", "csrc", "paged_attn.hip")
 
 
-def workload_work(wl, cached_len):
-    """Algorithmic FLOPs and bytes of one prefill attention launch."""
+def workload_work(wl, cached_len, tables):
+    """Algorithmic FLOPs and bytes of one prefill attention launch.
+
+    FLOPs count the visible (query, key) pairs only: 4 * Hq * D per pair (the
+    QK^T and PV products).  Logical bytes read every request's K/V context
+    once per request (shared prefix blocks once per request that holds them)
+    plus Q in and O out.  Unique bytes count each physical K/V block once, at
+    the largest number of its 16 slots any request reads, plus Q and O.
+    """
     sp = wl.spec
     L = wl.seq_lens.astype(np.float64)
     P = np.asarray(cached_len, dtype=np.float64)
     S = L - P
     pairs = float(np.sum(S * P + S * (S + 1) / 2))   # visible (query, key) pairs
     flops = 4.0 * sp.n_q_heads * sp.head_dim * pairs
-    kv_bytes = float(np.sum(4.0 * sp.n_kv_heads * sp.head_dim * L))   # K + V context, bf16
+    per_token = 4.0 * sp.n_kv_heads * sp.head_dim           # K + V of one token, bf16
+    kv_bytes = float(np.sum(per_token * L))
     qo_bytes = float(np.sum(4.0 * sp.n_q_heads * sp.head_dim * S))     # Q in + O out, bf16
+    Li = wl.seq_lens.astype(np.int64)
+    nb = (Li + 15) // 16
+    ids = np.concatenate([tables[r, :nb[r]] for r in range(len(Li))]).astype(np.int64)
+    fill = np.concatenate([np.minimum(16, Li[r] - 16 * np.arange(nb[r])) for r in range(len(Li))])
+    slots = np.zeros(int(ids.max()) + 1 if ids.size else 0, np.int64)
+    np.maximum.at(slots, ids, fill)
+    unique_kv = float(slots.sum()) * per_token
     return {"pairs": pairs, "flops": flops, "logical_bytes": kv_bytes + qo_bytes,
-            "query_tokens": int(S.sum())}
+            "unique_bytes": unique_kv + qo_bytes, "query_tokens": int(S.sum())}
 
 
 def kernel_source_sha() -> str:
@@ -99,48 +125,102 @@ def traffic_from_profile(workload_name: str):
     return float(fields["hbm_bytes_per_launch"]) if "hbm_bytes_per_launch" in fields else None
 
 
-def cpu_baseline(wl, cached_len, budget_s: float):
-    """Time the fp64 oracle (prefix match of the whole batch + attention of
-    requests in a seeded order, passing over the batch again while the budget
-    lasts) on the host cores."""
+def host_cpu():
+    """The host's processor as lscpu reports it, and the CPUs this process may use."""
+    info = {"nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0))}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+    except (OSError, subprocess.SubprocessError):
+        return info
+    keep = {"Model name": "model", "CPU(s)": "cpus", "Thread(s) per core": "threads_per_core",
+            "Core(s) per socket": "cores_per_socket", "Socket(s)": "sockets"}
+    for ln in out.splitlines():
+        k, _, v = ln.partition(":")
+        if k.strip() in keep:
+            info[keep[k.strip()]] = v.strip()
+    return info
+
+
+def cpu_baseline(wl, cached_len, work, n_tokens, budget_s: float, decode_budget_s: float):
+    """Time the fp64 oracle on the host cores and extrapolate it to the step.
+
+    Prefix match of the whole batch (timed in full), prefill attention of
+    requests in a seeded order until ``budget_s`` (passing over the batch again
+    if it is done first), and, for workloads with decode steps, seeded
+    (request, step) decode queries until ``decode_budget_s``.  The attention
+    parts are scaled to the whole step by FLOP ratio (their cost is
+    proportional to the visible pairs); the result is query tokens per second
+    of the whole step, prefill and decode tokens, like ``value``.
+    """
     from threadpoolctl import threadpool_info
 
-    from oracle.attn_ref import prefill_attention_ref
+    from oracle.attn_ref import decode_step_ref, prefill_attention_ref
     from oracle.prefix_ref import PrefixCacheRef
 
+    sp = wl.spec
     ref = PrefixCacheRef(1 << 30, 1 << 30)
     if wl.warm:
         ref.match(wl.warm)
+    dec = sp.decode_steps
+    reserve = [dec] * len(wl.prompts) if dec else None
     t0 = time.perf_counter()
-    c_ref, _, _ = ref.match(wl.prompts)
+    c_ref, _, _ = ref.match(wl.prompts, reserve=reserve)
     t_match = time.perf_counter() - t0
     assert np.array_equal(c_ref, cached_len)
+    per_pair = 4.0 * sp.n_q_heads * sp.head_dim
     rng = np.random.default_rng(0)
     order = rng.permutation(len(wl.prompts))
-    t_attn, tokens, done = 0.0, 0, 0
+    t_attn, flops_done, tokens, done = 0.0, 0.0, 0, 0
     for i in range(len(order) * 1000):
-        r = order[i % len(order)]
+        r = int(order[i % len(order)])
         L, P = int(wl.seq_lens[r]), int(cached_len[r])
-        k, v = wl.dense_kv(int(r), L)
-        q = wl.q_rows(int(r), P, L).float().cpu().numpy().astype(np.float64)
+        k, v = wl.dense_kv(r, L)
+        q = wl.q_rows(r, P, L).float().cpu().numpy().astype(np.float64)
         k = k.float().cpu().numpy().astype(np.float64)
         v = v.float().cpu().numpy().astype(np.float64)
         t0 = time.perf_counter()
-        prefill_attention_ref(q, k, v, wl.spec.scale)
+        prefill_attention_ref(q, k, v, sp.scale)
         t_attn += time.perf_counter() - t0
-        tokens += L - P
+        S = L - P
+        flops_done += per_pair * (S * P + S * (S + 1) / 2)
+        tokens += S
         done += 1
         if t_attn >= budget_s:
             break
-    total_q = int(np.sum(wl.seq_lens - cached_len))
-    sec_per_token = t_match / total_q + t_attn / tokens
+    t_prefill = t_attn * work["flops"] / flops_done
+    sample = (f"fp64 oracle: prefix match of all {len(wl.prompts)} prompts ({t_match * 1e3:.1f} ms, timed in full); "
+              f"prefill attention of {done} request passes in a seeded order ({tokens} query tokens, "
+              f"{t_attn:.1f} s) scaled by FLOP ratio {work['flops'] / flops_done:.3g} to the batch "
+              f"({t_prefill:.1f} s)")
+    t_decode = 0.0
+    if dec:
+        L_all = wl.seq_lens.astype(np.int64)
+        total = per_pair * float(np.sum(dec * (L_all + 1) + dec * (dec - 1) / 2))
+        t_dec, f_dec, n_dec = 0.0, 0.0, 0
+        picks = rng.permutation(len(wl.prompts))
+        for r in picks:
+            r = int(r)
+            s = int(rng.integers(0, dec))
+            n = int(L_all[r]) + s + 1
+            k, v = wl.dense_kv(r, n)
+            qd = wl.q_rows(r, n - 1, n)[0].float().cpu().numpy().astype(np.float64)
+            k = k.float().cpu().numpy().astype(np.float64)
+            v = v.float().cpu().numpy().astype(np.float64)
+            t0 = time.perf_counter()
+            decode_step_ref(qd, k, v, sp.scale)
+            t_dec += time.perf_counter() - t0
+            f_dec += per_pair * n
+            n_dec += 1
+            if t_dec >= decode_budget_s:
+                break
+        t_decode = t_dec * total / f_dec
+        sample += (f"; {n_dec} decode queries at seeded (request, step) ({t_dec:.2f} s) scaled by FLOP ratio "
+                   f"{total / f_dec:.3g} to {dec} steps x {len(wl.prompts)} prompts ({t_decode:.1f} s)")
+    t_step = t_match + t_prefill + t_decode
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] + [1])
-    return {"value": 1.0 / sec_per_token, "unit": "query tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": (f"fp64 oracle: prefix match of all {len(wl.prompts)} prompts ({t_match*1e3:.1f} ms) + "
-                       f"attention of {done} requests of the {len(wl.prompts)} in a seeded order, "
-                       f"repeated once the batch is done ({tokens} query tokens, {t_attn:.1f} s); "
-                       f"host nproc={os.cpu_count()}")}
+    return {"value": round(n_tokens / t_step, 2), "unit": "query tokens/s", "cores": int(threads),
+            "kind": "oracle", "extrapolated": bool(work["flops"] > flops_done or dec > 0),
+            "est_step_s": round(t_step, 6), "sample": sample, "host": host_cpu()}
 
 
 def icl_stream_workload(name: str, pair: bool):
@@ -173,10 +253,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama8b")
+    ap.add_argument("--workload", default="large")
     ap.add_argument("--prompts", type=int, default=0,
                     help="run the workload's shapes with this many prompts (0: its own count)")
-    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle attention to time")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle prefill attention to time")
+    ap.add_argument("--cpu-decode-budget", type=float, default=2.0,
+                    help="seconds of oracle decode queries to time (workloads with decode steps)")
+    ap.add_argument("--flush-mib", type=int, default=0,
+                    help="before every step, write this many MiB of device memory (evicts the MALL "
+                         "and L2 between steps; the write is inside the step time, outside the "
+                         "kernel timings)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-pair", action="store_true",
                     help="ICL stream workloads: serve the selector's demonstration order unrefined")
@@ -287,15 +373,22 @@ def main():
         torch.cuda.synchronize()
         dgraph = DecodeGraph(pc, tables, L, dec_in, dec_out, sp.scale)
         torch.cuda.synchronize()
-    work = workload_work(wl, cached)
+    work = workload_work(wl, cached, tables)
     n_tokens = work["query_tokens"] + dec * len(L)
 
     n_ev = args.steps + args.warmup
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
+    # decode attention launches, timed apart from their appends and uploads
+    n_dev = dec if dgraph is None else 0
+    dev_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n_dev)] for _ in range(n_ev)]
+    flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev) if args.flush_mib else None
     host_s = []
 
     def step(i):
         e = ev[i]
+        if flush is not None:
+            flush.fill_(i & 0xFF)
         h0 = time.perf_counter()
         m = pc.cache.checkpoint()
         c, t = pc.match(packed=(tokens, cu_tok), reserve=reserve)
@@ -329,10 +422,12 @@ def main():
                 qd = dec_rot[s]
             else:
                 pc.append(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], stream)
+            dev_ev[i][s][0].record(stream)
             if args.cascade:
                 pc.attend_cascade(bd, qd, dec_out[s], sp.scale, shared_len, decode_ws, stream)
             else:
                 pc.attend(bd, qd, dec_out[s], sp.scale, stream)
+            dev_ev[i][s][1].record(stream)
         e[3].record(stream)
         return c
 
@@ -354,16 +449,37 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
     tflops = work["flops"] / (attn_ms * 1e-3) / 1e12
     gbs = work["logical_bytes"] / (attn_ms * 1e-3) / 1e9
-    # the prefill launch is bound by whichever roofline limit is higher for it
+    unique_gbs = work["unique_bytes"] / (attn_ms * 1e-3) / 1e9
+    # roofline of the prefill launch: t_roof = max(FLOPs / MFMA peak, unique bytes / HBM peak);
+    # the launch is bound by whichever term is larger
     t_mfma = work["flops"] / (PEAK_BF16_TFLOPS * 1e12)
-    t_hbm = work["logical_bytes"] / (PEAK_HBM_GBS * 1e9)
+    t_hbm = work["unique_bytes"] / (PEAK_HBM_GBS * 1e9)
     traffic = None if args.prompts else traffic_from_profile(args.workload)
     if t_mfma >= t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic}
     else:
-        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic}
+        roof = {"bound": "hbm", "achieved": round(unique_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(unique_gbs / PEAK_HBM_GBS, 4), "traffic": traffic}
+    attn = {"launch_us": round(attn_ms * 1e3, 2), "tflops": round(tflops, 2),
+            "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "flops": work["flops"], "logical_bytes": work["logical_bytes"], "unique_bytes": work["unique_bytes"],
+            "logical_gbs": round(gbs, 1), "logical_hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+            "unique_gbs": round(unique_gbs, 1), "t_mfma_us": round(t_mfma * 1e6, 2),
+            "t_unique_hbm_us": round(t_hbm * 1e6, 2), "roofline_frac": round(max(t_mfma, t_hbm) / (attn_ms * 1e-3), 4),
+            "kernel_sha": kernel_source_sha()}
+    decode = None
+    if n_dev:
+        per = np.array([[a.elapsed_time(b) for (a, b) in e] for e in dev_ev[args.warmup:]])   # [steps, dec] ms
+        Ld = wl.seq_lens.astype(np.float64)
+        kv = 4.0 * sp.n_kv_heads * sp.head_dim
+        qo = 4.0 * sp.n_q_heads * sp.head_dim * len(Ld)
+        bytes_step = np.array([kv * float(np.sum(Ld + s + 1)) + qo for s in range(dec)])
+        us = per.mean(axis=0) * 1e3
+        dgbs = float(np.mean(bytes_step / (us * 1e-6) / 1e9))
+        decode = {"attn_us_per_step": round(float(us.mean()), 2), "bytes_per_step": float(bytes_step.mean()),
+                  "logical_gbs": round(dgbs, 1), "hbm_frac": round(dgbs / PEAK_HBM_GBS, 4),
+                  "flush_mib": args.flush_mib}
 
     line = {
         "metric": METRIC,
@@ -386,18 +502,19 @@ def main():
                    **({"chunk_tokens": args.chunk_tokens, "chunks": n_chunks} if args.chunk_tokens else {}),
                    **({"rope_base": args.rope} if args.rope else {}),
                    **({"decode_graph": True} if dgraph is not None else {}),
+                   **({"flush_mib": args.flush_mib} if args.flush_mib else {}),
                    **(icl or {})},
         "roofline": {**roof, **({"scope": f"all {n_chunks} chunked steps: appends, attention and the "
                                          "host's per-step metadata copies"} if args.chunk_tokens else {})},
-        "attn": {"launch_us": round(attn_ms * 1e3, 2), "tflops": round(tflops, 2),
-                 "logical_gbs": round(gbs, 1), "flops": work["flops"], "logical_bytes": work["logical_bytes"],
-                 "kernel_sha": kernel_source_sha()},
+        "attn": attn,
+        **({"decode_attn": decode} if decode else {}),
         "breakdown_ms": {"host_match_upload": round(float(np.mean(host_s)) * 1e3, 4),
                          "kv_append": round(append_ms, 4), "attention": round(attn_ms, 4),
                          "decode_steps": round(decode_ms, 4)},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, cached, args.cpu_budget)
+        line["cpu_baseline"] = cpu_baseline(wl, cached, work, n_tokens, args.cpu_budget,
+                                            args.cpu_decode_budget)
     print(json.dumps(line), flush=True)
 
 

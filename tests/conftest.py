@@ -15,3 +15,16 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def repo_root():
     return ROOT
+
+
+# Parity checks record one line each (workload, requests, max and mean absolute
+# error against the oracle); the lines are printed after the test summary, so
+# they appear in quiet runs too.
+PARITY_LINES: list = []
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    if PARITY_LINES:
+        terminalreporter.section("parity against the fp64 oracle")
+        for line in PARITY_LINES:
+            terminalreporter.write_line(line)

@@ -1,0 +1,74 @@
+"""The benchmark's algorithmic work model (CPU only): visible pairs, FLOPs,
+logical and unique bytes of a prefill launch, checked against brute-force
+counts over the host prefix match's block tables."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2507_08523_amd import ilpc, workload
+
+import bench
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ilpc.LIB_PATH):
+        pytest.fail("libilpc.so is not built: run `python -m paper_2507_08523_amd.build`")
+    return ilpc.load()
+
+
+def _match(wl):
+    cache = ilpc.PrefixCache(1 << 20, 22)
+    mb = max(-(-(len(p) + wl.spec.decode_steps) // 16) for p in wl.prompts)
+    if wl.warm:
+        cache.match(wl.warm, max_blocks=max(-(-len(p) // 16) for p in wl.warm))
+    res = [wl.spec.decode_steps] * len(wl.prompts) if wl.spec.decode_steps else None
+    c, t, _ = cache.match(wl.prompts, reserve=res, max_blocks=mb)
+    return c, t
+
+
+def _brute(wl, c, t):
+    sp = wl.spec
+    pairs = 0
+    slots = {}
+    for r, p in enumerate(wl.prompts):
+        L, P = len(p), int(c[r])
+        for i in range(P, L):          # query at absolute position i sees keys 0..i
+            pairs += i + 1
+        for pos in range(L):           # every key slot the request reads
+            b = int(t[r, pos // 16])
+            slots.setdefault(b, set()).add(pos % 16)
+    kv_tok = 4 * sp.n_kv_heads * sp.head_dim
+    qo = 4 * sp.n_q_heads * sp.head_dim * int(sum(len(p) for p in wl.prompts) - c.sum())
+    logical = kv_tok * sum(len(p) for p in wl.prompts) + qo
+    unique = kv_tok * sum(max(s) + 1 for s in slots.values()) + qo
+    return pairs, logical, unique
+
+
+@pytest.mark.parametrize("spec", [workload.SPECS["tiny"], workload.scaled_spec("llama8b", 12),
+                                  workload.scaled_spec("sweep100", 6), workload.scaled_spec("large", 3),
+                                  workload.scaled_spec("qwen7b", 5)])
+def test_work_model_matches_brute_force(lib, spec):
+    wl = workload.build(spec)
+    c, t = _match(wl)
+    w = bench.workload_work(wl, c, t)
+    pairs, logical, unique = _brute(wl, c, t)
+    assert w["pairs"] == pairs
+    assert w["flops"] == 4 * spec.n_q_heads * spec.head_dim * pairs
+    assert w["logical_bytes"] == logical
+    assert w["unique_bytes"] == unique
+    assert w["unique_bytes"] <= w["logical_bytes"]
+
+
+def test_sweep100_unique_bytes_count_the_shared_prefix_once(lib):
+    # 128 prompts share 976 tokens (61 blocks); each has 3 private blocks of
+    # its 48-token query: logical bytes read the prefix 128 times, unique once
+    wl = workload.build("sweep100")
+    c, t = _match(wl)
+    w = bench.workload_work(wl, c, t)
+    kv_tok = 4 * 8 * 128
+    qo = 4 * 32 * 128 * 128 * 48
+    assert w["logical_bytes"] == kv_tok * 128 * 1024 + qo
+    assert w["unique_bytes"] == kv_tok * (976 + 128 * 48) + qo
+    assert abs(w["unique_bytes"] / 1e6 - 130) < 1 and abs(w["logical_bytes"] / 1e6 - 638) < 1

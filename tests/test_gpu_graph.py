@@ -28,8 +28,11 @@ def _gpu():
 
 
 def log(*a):
+    import conftest
+
     print(*a, flush=True)
     sys.stdout.flush()
+    conftest.PARITY_LINES.append(" ".join(str(x) for x in a))
 
 
 # 16 prompts x 8 kv heads = 128 pairs (fewer than the compute units: the

@@ -4,9 +4,12 @@ Tolerance on bf16 attention outputs: max |err| <= 2e-2 and mean |err| <= 2e-3
 against the float64 oracle on the same bf16 inputs.  Prefix lengths and block
 tables are compared bit-exactly, K/V appends by exact read-back.
 
-Small workloads are checked in full; the large ones run at full size in the
-same launch configuration the benchmark times, and sampled requests (the
-extremes of cached length and query length plus seeded picks) are checked.
+Every workload runs at full size in the launch configuration the benchmark
+times.  tiny, llama8b, the ICL stream batches and every hit-rate sweep point
+are checked on every request; qwen7b and large on a fixed seeded set of 16
+requests (the extremes of cached length P and query length S, then seeded
+picks) over all heads, and large's 32 decode steps on those 16 requests at
+every step.  Each check logs its max and mean absolute error.
 """
 import sys
 
@@ -34,8 +37,11 @@ def _gpu():
 
 
 def log(*a):
+    import conftest
+
     print(*a, flush=True)
     sys.stdout.flush()
+    conftest.PARITY_LINES.append(" ".join(str(x) for x in a))
 
 
 class Run:
@@ -117,6 +123,36 @@ def _sample(run, n_rand, seed=0):
     return sorted(picks)
 
 
+def _pick(run, n, seed=0):
+    """A fixed seeded set of n requests: the extremes of cached length P and
+    of query length S first (argmin/argmax of each), then seeded picks."""
+    c = run.cached
+    S = run.wl.seq_lens - c
+    picks = []
+    for r in (np.argmax(S), np.argmin(c), np.argmax(c), np.argmin(S)):
+        if int(r) not in picks:
+            picks.append(int(r))
+    for r in np.random.default_rng(seed).permutation(len(c)):
+        if len(picks) == n:
+            break
+        if int(r) not in picks:
+            picks.append(int(r))
+    return picks
+
+
+# Full-size runs are kept between the tests that check parts of them; only one
+# is held at a time (the large batch needs about 60 GB of device memory).
+_RUNS: dict = {}
+
+
+def _full_run(name):
+    if name not in _RUNS:
+        _RUNS.clear()
+        torch.cuda.empty_cache()
+        _RUNS[name] = Run(name)
+    return _RUNS[name]
+
+
 @pytest.mark.parametrize("name", ["tiny", "llama8b"])
 def test_prefill_full_check(name):
     run = Run(name)
@@ -138,45 +174,83 @@ def test_icl_stream_batch_full_check(pair):
     run.check(range(len(run.wl.prompts)), tag=" pair" if pair else " naive")
 
 
-def test_qwen7b_full_size_sampled():
-    run = Run("qwen7b")
+def test_qwen7b_full_size_16_requests():
+    run = _full_run("qwen7b")
     assert (run.wl.seq_lens - run.cached).min() >= 20
-    run.check(_sample(run, 4))
+    picks = _pick(run, 16)
+    assert len(picks) == 16
+    run.check(picks, tag=" 16 requests")
 
 
-@pytest.mark.parametrize("name", ["sweep0", "sweep25", "sweep50", "sweep75", "sweep100"])
-def test_sweep_full_size_sampled(name):
-    run = Run(name)
+SWEEP_PARTS = 4
+
+
+@pytest.mark.parametrize("name,part", [(f"sweep{p}", i) for p in (0, 25, 50, 75, 100)
+                                       for i in range(SWEEP_PARTS)])
+def test_sweep_full_size_every_request(name, part):
+    """Every one of the 128 requests of each hit-rate sweep point, in four
+    parts of 32 (one full-size launch per point)."""
+    run = _full_run(name)
     expect = {"sweep0": 0, "sweep25": 256, "sweep50": 496, "sweep75": 736, "sweep100": 976}[name]
     assert (run.cached == expect).all()
-    run.check(_sample(run, 3))
+    B = len(run.wl.prompts)
+    assert B == 128
+    n = B // SWEEP_PARTS
+    run.check(range(part * n, (part + 1) * n), tag=f" requests {part * n}..{(part + 1) * n - 1}")
 
 
-def test_large_prefill_then_decode_sampled():
-    run = Run("large")
+LARGE_PICKS, LARGE_PARTS = 16, 8
+
+
+@pytest.mark.parametrize("part", range(LARGE_PARTS))
+def test_large_prefill_16_requests(part):
+    """The large batch (512 prompts x 2112 tokens, 64 q / 8 kv heads) at full
+    size: 16 seeded requests spanning min/max P and S, all heads, in parts."""
+    run = _full_run("large")
+    picks = _pick(run, LARGE_PICKS)
+    assert len(picks) == LARGE_PICKS
+    n = LARGE_PICKS // LARGE_PARTS
+    run.check(picks[part * n:(part + 1) * n], tag=f" prefill picks {part * n}..{(part + 1) * n - 1}")
+
+
+def test_large_decode_every_step_16_requests():
+    """32 decode steps of the whole large batch (one query per prompt over the
+    grown context); the same 16 requests checked at every step."""
+    run = _full_run("large")
     wl, pc = run.wl, run.pc
-    picks = _sample(run, 1)
-    run.check(picks[:3])
-    B = len(wl.prompts)
+    picks = _pick(run, LARGE_PICKS)
+    B, steps = len(wl.prompts), wl.spec.decode_steps
+    assert steps == 32
     L = wl.seq_lens.astype(np.int32)
     cu = np.arange(B + 1, dtype=np.int32)
-    worst = 0.0
-    for s in range(wl.spec.decode_steps):
+    dense = {}
+    for r in picks:
+        k, v = wl.dense_kv(r, int(L[r]) + steps)
+        dense[r] = (k.float().cpu().numpy(), v.float().cpu().numpy())
+    worst, tot, cnt = 0.0, 0.0, 0
+    for s in range(steps):
         d = wl.decode_inputs(s)
         b = pc.upload(run.tables, cu, L + s + 1, L + s)
         pc.append(b, d["k_new"], d["v_new"])
         out = torch.empty_like(d["q"])
         pc.attend(b, d["q"], out, wl.spec.scale)
-        if s in (0, 13, wl.spec.decode_steps - 1):
-            torch.cuda.synchronize()
-            for r in picks:
-                k, v = wl.dense_kv(r, int(L[r]) + s + 1)
-                ref = decode_step_ref(d["q"][r].float().cpu().numpy(), k.float().cpu().numpy(),
-                                      v.float().cpu().numpy(), wl.spec.scale)
-                err = np.abs(out[r].float().cpu().numpy() - ref)
-                worst = max(worst, float(err.max()))
-                assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (s, r)
-    log(f"[parity] large decode: 32 steps, sampled max_abs={worst:.3e}")
+        torch.cuda.synchronize()
+        got_all = out.float().cpu().numpy()
+        q_all = d["q"].float().cpu().numpy()
+        for r in picks:
+            n = int(L[r]) + s + 1
+            k, v = dense[r]
+            ref = decode_step_ref(q_all[r], k[:n], v[:n], wl.spec.scale)
+            err = np.abs(got_all[r] - ref)
+            assert np.isfinite(got_all[r]).all(), (s, r)
+            worst = max(worst, float(err.max()))
+            tot += float(err.sum())
+            cnt += err.size
+            assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (s, r)
+    log(f"[parity] large decode: {steps} steps x {len(picks)} requests max_abs={worst:.3e} "
+        f"mean_abs={tot / cnt:.3e}")
+    _RUNS.clear()
+    torch.cuda.empty_cache()
 
 
 def test_kv_append_read_back_bit_exact():

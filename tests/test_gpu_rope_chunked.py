@@ -33,8 +33,11 @@ def _gpu():
 
 
 def log(*a):
+    import conftest
+
     print(*a, flush=True)
     sys.stdout.flush()
+    conftest.PARITY_LINES.append(" ".join(str(x) for x in a))
 
 
 def _setup(name, n_prompts, base=None):
