@@ -39,7 +39,8 @@ append (ilpc_rope_kv_append; the warm prefix is rotated the same way).
 tokens (append + attention per step); the attention timing and ``roofline``
 then cover all steps.  ``--graph`` (decode workloads) captures the 32 decode
 steps once as a HIP graph with all their metadata on the device, and every
-timed step replays it.  ``--prompts N`` keeps the workload's shapes with N
+timed step replays it; with ``--chunk-tokens`` it also captures the
+scheduler steps of the chunked prefill as one graph.  ``--prompts N`` keeps the workload's shapes with N
 prompts (``large --prompts 16``: decode steps of a small batch, whose
 attention splits each request's keys over several waves).
 
@@ -271,7 +272,8 @@ def main():
     ap.add_argument("--rope", type=float, default=0.0, metavar="BASE",
                     help="rotate new K and Q with RoPE of this base inside the append (0: off)")
     ap.add_argument("--graph", action="store_true",
-                    help="decode workloads: replay the decode steps as one captured HIP graph")
+                    help="replay the decode steps (decode workloads) and the chunked prefill steps "
+                         "(--chunk-tokens) as captured HIP graphs")
     ap.add_argument("--cascade", action="store_true",
                     help="split the prefill attention at the prefix every prompt shares")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -285,8 +287,8 @@ def main():
     import torch
 
     from paper_2507_08523_amd import ilpc, workload
-    from paper_2507_08523_amd.pipeline import (DecodeGraph, PagedPrefixCache, chunk_schedule, max_blocks_of,
-                                               pool_blocks_needed, rope_inv_freq, shared_prefix_len)
+    from paper_2507_08523_amd.pipeline import (ChunkGraph, DecodeGraph, PagedPrefixCache, chunk_schedule,
+                                               max_blocks_of, pool_blocks_needed, rope_inv_freq, shared_prefix_len)
 
     ilpc.load()
     dev = torch.device("cuda:0")
@@ -319,8 +321,8 @@ def main():
     if args.cascade and (args.rope or args.chunk_tokens):
         print("--cascade does not combine with --rope or --chunk-tokens", file=sys.stderr)
         sys.exit(2)
-    if args.graph and (args.cascade or args.rope):
-        print("--graph does not combine with --cascade or --rope", file=sys.stderr)
+    if args.graph and (args.cascade or (args.rope and sp.decode_steps)):
+        print("--graph does not combine with --cascade, nor with --rope on decode workloads", file=sys.stderr)
         sys.exit(2)
     inv_freq = torch.from_numpy(rope_inv_freq(sp.head_dim, args.rope)).to(dev) if args.rope else None
 
@@ -365,7 +367,13 @@ def main():
     dec_out = [torch.empty_like(d["q"]) for d in dec_in]
     dec_rot = [torch.empty_like(d["q"]) for d in dec_in] if args.rope else None
     cu_dec = np.arange(len(L) + 1, dtype=np.int32)
-    dgraph = None
+    dgraph = cgraph = None
+    if args.graph and args.chunk_tokens:
+        # all scheduler steps of the chunked prefill as one graph (its eager
+        # pass also leaves the prefill's K/V in the pools)
+        cgraph = ChunkGraph(pc, cached, tables, L, q, k_new, v_new, out, sp.scale, args.chunk_tokens, inv_freq,
+                            q_rot)
+        torch.cuda.synchronize()
     if args.graph and dec:
         # the prefill's K/V must be in the pools before the eager pass of the capture
         b = pc.upload_prefill(cached, tables, L, stream)
@@ -396,7 +404,11 @@ def main():
         pc.cache.rollback(m)
         host_s.append(time.perf_counter() - h0)
         e[0].record(stream)
-        if args.chunk_tokens:   # appends and attention interleave, chunk by chunk
+        if cgraph is not None:   # every scheduler step, replayed as one graph
+            assert np.array_equal(t, tables), "block tables changed since the capture"
+            e[1].record(stream)
+            cgraph.replay()
+        elif args.chunk_tokens:   # appends and attention interleave, chunk by chunk
             e[1].record(stream)
             pc.prefill_chunked(c, t, L, q, k_new, v_new, out, sp.scale, args.chunk_tokens, stream,
                                inv_freq, q_rot)
@@ -502,6 +514,7 @@ def main():
                    **({"chunk_tokens": args.chunk_tokens, "chunks": n_chunks} if args.chunk_tokens else {}),
                    **({"rope_base": args.rope} if args.rope else {}),
                    **({"decode_graph": True} if dgraph is not None else {}),
+                   **({"chunk_graph": True} if cgraph is not None else {}),
                    **({"flush_mib": args.flush_mib} if args.flush_mib else {}),
                    **(icl or {})},
         "roofline": {**roof, **({"scope": f"all {n_chunks} chunked steps: appends, attention and the "

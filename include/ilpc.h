@@ -22,7 +22,8 @@
  *     failing call leaves the cache unchanged; its outputs are unspecified.
  *   - Host pointers are marked [host], device pointers [device].  The caller
  *     owns every buffer (including the attention workspace); the library owns
- *     only the cache handle (host memory) and allocates no device memory.
+ *     only the cache and ICL-table handles (host memory) and allocates no
+ *     device memory.
  *   - bf16 tensors are passed as uint16_t* holding the raw bf16 bits.
  *   - `stream` is a hipStream_t (NULL = the null stream).  Device calls are
  *     asynchronous on that stream; they return ILPC_EHIP when the launch
@@ -360,6 +361,48 @@ int ilpc_paged_prefill_attn_cascade(const uint16_t* q, const uint16_t* k_pool, c
                                     int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
                                     int32_t block_size, int32_t shared_len, float softmax_scale,
                                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Scheduler steps of a chunked prefill (the per-step token bound that section
+ * 3.3 tunes, vLLM's max-num-batched-tokens; section 4.1's PC-Chunk baseline).
+ * Host only.
+ *
+ * q_lens      [host] int32 [B]  new (uncached) tokens of each request, >= 0
+ * budget      new tokens per step, >= 1
+ * max_pieces  room of the four piece arrays
+ * piece_req, piece_off, piece_len, piece_step  [host] int32 [max_pieces]
+ *             out: piece k is tokens piece_off[k] .. piece_off[k] +
+ *             piece_len[k] - 1 of request piece_req[k]'s new tokens, run in
+ *             step piece_step[k]
+ * n_pieces, n_steps  out: the number of pieces and of steps (also set when
+ *             the pieces do not fit, so a call with max_pieces = 0 sizes them)
+ *
+ * First come, first served over the requests in order: a step takes what is
+ * left of the current request, then the following ones, and cuts the last
+ * one it reaches, so every step but the last holds exactly `budget` tokens
+ * and a step is a contiguous run of the batch's packed new-token rows.
+ * Pieces come in step order and, within a step, request order; requests with
+ * no new tokens get none.  ILPC_EINVAL for a negative length, budget < 1, or
+ * pieces that do not fit in max_pieces.
+ */
+int ilpc_chunk_schedule(const int32_t* q_lens, int32_t B, int32_t budget, int32_t max_pieces,
+                        int32_t* piece_req, int32_t* piece_off, int32_t* piece_len, int32_t* piece_step,
+                        int32_t* n_pieces, int32_t* n_steps);
+
+/*
+ * Split point for ilpc_paged_prefill_attn_cascade: the keys at the front that
+ * every request of the batch shares (the instruction and leading
+ * demonstrations, section 2.1.1, stored once by the prefix cache, section
+ * 2.1.2).  Host only.
+ *
+ * cached_len   [host] int32 [B]              P_r of each request, >= 0
+ * block_tables [host] int32 [B, max_blocks]  as ilpc_prefix_match returned them
+ * shared_len   out: 16 * the longest run of leading block ids that are equal
+ *              (and >= 0) in every row, capped at floor(min_r P_r / 16)
+ *              blocks, so that the shared keys precede every query; 0 for B = 0.
+ */
+int ilpc_shared_prefix_len(const int32_t* cached_len, const int32_t* block_tables, int32_t B,
+                           int32_t max_blocks, int32_t* shared_len);
 
 /*
  * Prefix-aware refinement of in-context demonstrations (section 3.2.1,

@@ -16,6 +16,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libilpc.so")
 SOURCES = [os.path.join(PKG, "csrc", "prefix_cache.cpp"), os.path.join(PKG, "csrc", "pair_table.cpp"),
+           os.path.join(PKG, "csrc", "schedule.cpp"),
            os.path.join(PKG, "csrc", "paged_attn.hip"), os.path.join(PKG, "csrc", "rope_append.hip"),
            os.path.join(PKG, "csrc", "decode_attn.hip")]
 ARCH = "gfx950"

@@ -51,6 +51,9 @@ _SIGS = [
     ("ilpc_paged_prefill_attn_cascade", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32,
                                                _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                                ctypes.c_size_t, _vp]),
+    ("ilpc_chunk_schedule", _i32, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_i32),
+                                   ctypes.POINTER(_i32)]),
+    ("ilpc_shared_prefix_len", _i32, [_vp, _vp, _i32, _i32, ctypes.POINTER(_i32)]),
     ("ilpc_cache_create_lru", _i32, [_i32, _i32, _i32, ctypes.POINTER(_vp)]),
     ("ilpc_cache_release", _i32, [_vp, _vp, _i32, _i32]),
     ("ilpc_cache_touch", _i32, [_vp, _vp, _i32]),
@@ -236,6 +239,43 @@ class PairTable:
         d = np.zeros_like(t)
         _check(load().ilpc_pair_entries(self._h, _np_ptr(t), _np_ptr(d), cap, ctypes.byref(n)))
         return t[:n.value].copy(), d[:n.value].copy()
+
+
+# -- host scheduling policy ---------------------------------------------------
+
+def chunk_schedule(q_lens, budget: int):
+    """Scheduler steps of at most ``budget`` new tokens (ilpc_chunk_schedule).
+
+    Returns, per step, a list of (request, offset into its new tokens, count).
+    """
+    q = np.ascontiguousarray(q_lens, dtype=np.int32)
+    B = int(q.shape[0])
+    lib = load()
+    n_p, n_s = _i32(), _i32()
+    rc = lib.ilpc_chunk_schedule(_np_ptr(q), B, int(budget), 0, None, None, None, None,
+                                 ctypes.byref(n_p), ctypes.byref(n_s))
+    if rc != OK and n_p.value == 0:
+        _check(rc)
+    n = n_p.value
+    req, off, ln, st = (np.empty(max(n, 1), np.int32) for _ in range(4))
+    _check(lib.ilpc_chunk_schedule(_np_ptr(q), B, int(budget), n, _np_ptr(req), _np_ptr(off), _np_ptr(ln),
+                                   _np_ptr(st), ctypes.byref(n_p), ctypes.byref(n_s)))
+    steps = [[] for _ in range(n_s.value)]
+    for k in range(n):
+        steps[int(st[k])].append((int(req[k]), int(off[k]), int(ln[k])))
+    return steps
+
+
+def shared_prefix_len(cached_len, block_tables) -> int:
+    """Keys every request shares at the front (ilpc_shared_prefix_len)."""
+    c = np.ascontiguousarray(cached_len, dtype=np.int32)
+    t = np.ascontiguousarray(block_tables, dtype=np.int32)
+    B = int(c.shape[0])
+    if t.ndim != 2 or t.shape[0] != B:
+        raise ILPCError(EINVAL, "shared_prefix_len: block_tables must be [B, max_blocks]")
+    out = _i32()
+    _check(load().ilpc_shared_prefix_len(_np_ptr(c), _np_ptr(t), B, int(t.shape[1]), ctypes.byref(out)))
+    return int(out.value)
 
 
 # -- device steps ------------------------------------------------------------

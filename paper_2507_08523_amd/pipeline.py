@@ -189,37 +189,18 @@ class PagedPrefixCache:
         q, k_new, v_new, out: the batch's suffix rows, packed request by
         request (as for a single pass).  Step s covers packed rows
         [s * budget, (s + 1) * budget): the rest of one request, whole
-        requests, the head of another (first come, first served).  Each step
-        appends its rows' K/V and attends its queries over every key up to its
-        last row.  The metadata of all steps goes to the device in one copy,
-        so a step costs the host two launches.  With ``inv_freq`` the append
-        also rotates K and Q (into ``q_rot``, which attention then reads).
-        Returns the number of steps.
+        requests, the head of another (first come, first served; the
+        library's ilpc_chunk_schedule).  Each step appends its rows' K/V and
+        attends its queries over every key up to its last row.  The metadata
+        of all steps goes to the device in one copy, so a step costs the host
+        two launches (ChunkGraph replays them all as one).  With ``inv_freq``
+        the append also rotates K and Q (into ``q_rot``, which attention then
+        reads).  Returns the number of steps.
         """
-        cached_len = np.asarray(cached_len, dtype=np.int64)
-        q_lens = np.asarray(seq_lens, dtype=np.int64) - cached_len
-        steps = chunk_schedule(q_lens, budget)
-        meta = []
-        for step in steps:
-            rs = [r for (r, _, _) in step]
-            n = np.array([m for (_, _, m) in step], np.int64)
-            off = np.array([o for (_, o, _) in step], np.int64)
-            start = cached_len[rs] + off
-            cu = np.zeros(len(step) + 1, np.int32)
-            cu[1:] = np.cumsum(n)
-            meta.append((np.ascontiguousarray(tables[rs]), cu, (start + n).astype(np.int32),
-                         start.astype(np.int32)))
-        row = 0
-        for b in self.upload_steps(meta, stream):
-            rows = slice(row, row + b.total_q)
-            if inv_freq is None:
-                self.append(b, k_new[rows], v_new[rows], stream)
-                self.attend(b, q[rows], out[rows], scale, stream)
-            else:
-                self.append_rope(b, k_new[rows], v_new[rows], inv_freq, q[rows], q_rot[rows], stream)
-                self.attend(b, q_rot[rows], out[rows], scale, stream)
-            row += b.total_q
-        return len(steps)
+        meta = chunk_metadata(cached_len, tables, seq_lens, budget)
+        run_chunk_steps(self, self.upload_steps(meta, stream), q, k_new, v_new, out, scale, stream, inv_freq,
+                        q_rot)
+        return len(meta)
 
     def attend(self, batch: DeviceBatch, q, out, scale: float, stream=None):
         ilpc.paged_prefill_attn(q, self.k_pool, self.v_pool, batch.block_tables, batch.cu_q,
@@ -306,30 +287,114 @@ class DecodeGraph:
         self.graph.replay()
 
 
-def chunk_schedule(q_lens, budget: int):
-    """Scheduler steps of at most ``budget`` new tokens (max-num-batched-tokens).
+def chunk_metadata(cached_len, tables, seq_lens, budget: int) -> list:
+    """Per scheduler step of a chunked prefill: (block tables, cu_q, seq_lens,
+    start positions) of the pieces it runs, in the layout PagedPrefixCache.upload
+    takes.  A piece's queries attend to every key up to its last row."""
+    cached_len = np.asarray(cached_len, dtype=np.int64)
+    q_lens = np.asarray(seq_lens, dtype=np.int64) - cached_len
+    meta = []
+    for step in chunk_schedule(q_lens, budget):
+        rs = [r for (r, _, _) in step]
+        n = np.array([m for (_, _, m) in step], np.int64)
+        off = np.array([o for (_, o, _) in step], np.int64)
+        start = cached_len[rs] + off
+        cu = np.zeros(len(step) + 1, np.int32)
+        cu[1:] = np.cumsum(n)
+        meta.append((np.ascontiguousarray(tables[rs]), cu, (start + n).astype(np.int32), start.astype(np.int32)))
+    return meta
 
-    First come, first served over the batch's requests in order: a step takes
-    what is left of the current request, then the next requests, and cuts the
-    last one it reaches.  Returns, per step, a list of (request, offset into
-    its new tokens, count); requests with no new tokens are skipped.
+
+def run_chunk_steps(pc, batches, q, k_new, v_new, out, scale, stream=None, inv_freq=None, q_rot=None):
+    """Append + attention of every scheduler step, step after step on `stream`."""
+    row = 0
+    for b in batches:
+        rows = slice(row, row + b.total_q)
+        if inv_freq is None:
+            pc.append(b, k_new[rows], v_new[rows], stream)
+            pc.attend(b, q[rows], out[rows], scale, stream)
+        else:
+            pc.append_rope(b, k_new[rows], v_new[rows], inv_freq, q[rows], q_rot[rows], stream)
+            pc.attend(b, q_rot[rows], out[rows], scale, stream)
+        row += b.total_q
+
+
+def _device_batches(meta, max_blocks, device):
+    """All batches' metadata in one device buffer (one copy); DeviceBatch views."""
+    import torch
+
+    sizes = [int(t.shape[0]) * max_blocks + 3 * int(t.shape[0]) + 1 for (t, _, _, _) in meta]
+    host = np.empty(int(sum(sizes)), np.int32)
+    o = 0
+    for (tables, cu_q, seq_lens, start_pos), size in zip(meta, sizes):
+        B = int(tables.shape[0])
+        nbt = B * max_blocks
+        host[o:o + nbt] = np.asarray(tables).reshape(-1)
+        host[o + nbt:o + nbt + B + 1] = cu_q
+        host[o + nbt + B + 1:o + nbt + 2 * B + 1] = seq_lens
+        host[o + nbt + 2 * B + 1:o + size] = start_pos
+        o += size
+    d = torch.from_numpy(host).to(device)
+    out, o = [], 0
+    for (tables, cu_q, _, _), size in zip(meta, sizes):
+        B = int(tables.shape[0])
+        nbt = B * max_blocks
+        q_lens = np.diff(np.asarray(cu_q, dtype=np.int64))
+        out.append(DeviceBatch(block_tables=d[o:o + nbt].view(B, max_blocks), cu_q=d[o + nbt:o + nbt + B + 1],
+                               seq_lens=d[o + nbt + B + 1:o + nbt + 2 * B + 1],
+                               start_pos=d[o + nbt + 2 * B + 1:o + size],
+                               max_q_len=int(q_lens.max()) if B else 0, total_q=int(cu_q[-1]) if B else 0,
+                               B=B))
+        o += size
+    return d, out
+
+
+class ChunkGraph:
+    """The scheduler steps of a chunked prefill captured once as a HIP graph.
+
+    Every step (append of its rows' K/V, optionally rotated, then attention of
+    its queries) is recorded in order on one default-priority capture stream
+    and replayed as one launch, so the steps run back to back without the
+    host's two launches per step.  The steps' metadata lives in a device
+    buffer the graph owns; q, k_new, v_new, out (and q_rot) are the caller's
+    tensors, read and written at every replay.  Replays repeat the same
+    appends into the same slots, so they are idempotent.  Nothing in the
+    capture clears memory with a memset: the attention workspace is created
+    (zero-filled) before the capture and every attention call leaves its
+    counters zero.
     """
-    if budget < 1:
-        raise ilpc.ILPCError(ilpc.EINVAL, "chunk_schedule: budget < 1")
-    steps, cur, room = [], [], budget
-    for r, n in enumerate(np.asarray(q_lens, dtype=np.int64).tolist()):
-        off = 0
-        while off < n:
-            take = min(n - off, room)
-            cur.append((r, off, take))
-            off += take
-            room -= take
-            if room == 0:
-                steps.append(cur)
-                cur, room = [], budget
-    if cur:
-        steps.append(cur)
-    return steps
+
+    def __init__(self, pc: PagedPrefixCache, cached_len, tables, seq_lens, q, k_new, v_new, out, scale: float,
+                 budget: int, inv_freq=None, q_rot=None):
+        import torch
+
+        meta = chunk_metadata(cached_len, tables, seq_lens, budget)
+        self.n_steps = len(meta)
+        self.meta, self.batches = _device_batches(meta, pc.max_blocks, pc.device)
+        self.stream = torch.cuda.Stream(pc.device)
+        self.stream.wait_stream(torch.cuda.current_stream(pc.device))
+        Hq = q.shape[1]
+        need = max([ilpc.attn_workspace_bytes(b.B, b.max_q_len, Hq, pc.n_kv_heads, pc.head_dim)
+                    for b in self.batches] + [64])
+        ilpc.attn_workspace(pc.device, self.stream, need)
+        args = (pc, self.batches, q, k_new, v_new, out, scale, self.stream, inv_freq, q_rot)
+        run_chunk_steps(*args)                  # eager once on the capture stream
+        self.stream.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph, stream=self.stream):
+            run_chunk_steps(*args)
+
+    def replay(self):
+        """Launch every captured step on the current stream."""
+        self.graph.replay()
+
+
+def chunk_schedule(q_lens, budget: int):
+    """Scheduler steps of at most ``budget`` new tokens (max-num-batched-tokens):
+    first come, first served over the batch's requests, as the library's
+    ilpc_chunk_schedule computes them.  Returns, per step, a list of
+    (request, offset into its new tokens, count)."""
+    return ilpc.chunk_schedule(q_lens, budget)
 
 
 def rope_inv_freq(head_dim: int, base: float):
@@ -339,17 +404,10 @@ def rope_inv_freq(head_dim: int, base: float):
 
 
 def shared_prefix_len(cached_len, block_tables) -> int:
-    """Keys at the front that every request of a batch shares: the longest run of
-    leading block ids equal across all rows of the host block table, capped by
-    the shortest cached prefix (so the shared keys precede every query)."""
-    cached_len = np.asarray(cached_len)
-    t = np.asarray(block_tables)
-    if len(cached_len) == 0:
-        return 0
-    n = int(cached_len.min()) // BLOCK
-    same = (t[:, :n] == t[0, :n]).all(axis=0) & (t[0, :n] >= 0)
-    run = n if same.all() else int(np.argmin(same))
-    return run * BLOCK
+    """Keys at the front that every request of a batch shares (the library's
+    ilpc_shared_prefix_len): the longest run of leading block ids equal across
+    all rows of the host block table, capped by the shortest cached prefix."""
+    return ilpc.shared_prefix_len(cached_len, block_tables)
 
 
 # Sets the ICL table holds.  The paper sizes the table offline from the

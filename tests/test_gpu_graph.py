@@ -1,7 +1,9 @@
 """GPU: decode steps captured as a HIP graph (pipeline.DecodeGraph) replay to
 exactly the eager results, replay after replay with eager work in between,
 on both decode paths (the one-wave-per-pair kernel and the persistent kernel
-with its work-queue workspace), and agree with the fp64 oracle.
+with its work-queue workspace), and agree with the fp64 oracle.  The same
+holds for the scheduler steps of a chunked prefill (pipeline.ChunkGraph),
+with and without RoPE in the append.
 """
 import sys
 
@@ -91,3 +93,72 @@ def test_decode_graph_replays_equal_eager(n_prompts):
             worst = max(worst, float(err.max()))
             assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
     log(f"[graph] {sp.name}: {dec} captured decode steps, 3 replays equal to eager, oracle max_abs={worst:.3e}")
+
+
+@pytest.mark.parametrize("budget,rope", [(1024, False), (300, True)])
+def test_chunk_graph_replays_equal_eager(budget, rope):
+    """The steps of a chunked prefill captured as one graph (pipeline.ChunkGraph):
+    every replay equals the eager chunked run bit for bit, with eager work on
+    the default stream between replays, and agrees with the fp64 oracle."""
+    from oracle.attn_ref import prefill_attention_ref
+    from oracle.rope_ref import rope
+    from paper_2507_08523_amd.pipeline import ChunkGraph, rope_inv_freq
+
+    wl = workload.build(workload.scaled_spec("llama8b", 24))
+    wl.materialize("cuda")
+    sp = wl.spec
+    pc = PagedPrefixCache(sp.n_kv_heads, sp.head_dim, pool_blocks_needed(wl), max_blocks_of(wl),
+                          max(len(wl.prompts), len(wl.warm)), 16)
+    inv = torch.from_numpy(rope_inv_freq(sp.head_dim, 5e5)).cuda() if rope else None
+    c, t = pc.match(wl.warm)
+    rows = wl.packed_warm(c)
+    b = pc.upload_prefill(c, t, [len(p) for p in wl.warm])
+    if rope:
+        pc.append_rope(b, rows["k_new"], rows["v_new"], inv)
+    else:
+        pc.append(b, rows["k_new"], rows["v_new"])
+    c, t = pc.match(wl.prompts)
+    rows = wl.packed_suffix(c)
+    L = wl.seq_lens.astype(np.int32)
+    q, k_new, v_new = rows["q"], rows["k_new"], rows["v_new"]
+    q_rot = torch.empty_like(q) if rope else None
+    eager = torch.full_like(q, float("nan"))
+    n = pc.prefill_chunked(c, t, L, q, k_new, v_new, eager, sp.scale, budget, None, inv, q_rot)
+    torch.cuda.synchronize()
+    assert n == -(-int((L - c).sum()) // budget)
+    eager_rot = q_rot.clone() if rope else None
+
+    out = torch.empty_like(q)
+    g = ChunkGraph(pc, c, t, L, q, k_new, v_new, out, sp.scale, budget, inv, q_rot)
+    torch.cuda.synchronize()
+    assert g.n_steps == n
+    for rep in range(3):
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {rep} differs from the eager chunked run"
+        if rope:
+            assert torch.equal(q_rot, eager_rot)
+        # eager work on the default stream between replays
+        other = torch.empty_like(q)
+        pc.prefill_chunked(c, t, L, q, k_new, v_new, other, sp.scale, budget, None, inv, q_rot)
+        torch.cuda.synchronize()
+        assert torch.equal(other, eager)
+    worst = 0.0
+    for r in (0, len(L) // 2, len(L) - 1):
+        P, Lr = int(c[r]), int(L[r])
+        k, v = wl.dense_kv(r, Lr)
+        qr = wl.q_rows(r, P, Lr).float().cpu().numpy()
+        k = k.float().cpu().numpy()
+        v = v.float().cpu().numpy()
+        if rope:
+            f = inv.cpu().numpy()
+            qr = rope(qr, np.arange(P, Lr), f)
+            k = rope(k, np.arange(Lr), f)
+        ref = prefill_attention_ref(qr, k, v, sp.scale)
+        got = out[int(rows["cu"][r]):int(rows["cu"][r + 1])].float().cpu().numpy()
+        err = np.abs(got - ref)
+        assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, r
+        worst = max(worst, float(err.max()))
+    log(f"[graph] chunked prefill llama8b[24] budget {budget}{' rope' if rope else ''}: {n} steps, "
+        f"3 replays bit-identical, max_abs={worst:.3e}")
