@@ -22,8 +22,9 @@
  *     failing call leaves the cache unchanged; its outputs are unspecified.
  *   - Host pointers are marked [host], device pointers [device].  The caller
  *     owns every buffer (including the attention workspace); the library owns
- *     only the cache and ICL-table handles (host memory) and allocates no
- *     device memory.
+ *     the cache and ICL-table handles (host memory) and one static device
+ *     array (the scratch of ilpc_paged_prefill_attn_noalloc), and allocates
+ *     no device memory.
  *   - bf16 tensors are passed as uint16_t* holding the raw bf16 bits.
  *   - `stream` is a hipStream_t (NULL = the null stream).  Device calls are
  *     asynchronous on that stream; they return ILPC_EHIP when the launch
@@ -324,6 +325,33 @@ int ilpc_paged_prefill_attn(const uint16_t* q, const uint16_t* k_pool, const uin
                             int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
                             int32_t block_size, float softmax_scale, uint16_t* out,
                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ilpc_paged_prefill_attn without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  It allocates nothing: its
+ * workspace is a static device array of the library, 8 MiB + 256 bytes, one
+ * per GPU, held from its first use on that GPU until the process ends.  The
+ * first call on a device looks up that device's copy (with the device
+ * current); later calls reuse the address.
+ *
+ * Arguments, layouts, bounds rules and the result are those of
+ * ilpc_paged_prefill_attn with a workspace of 8 MiB + 256 bytes, and the
+ * kernels are the same: the first 64 bytes hold the work-queue counters
+ * (zero when the library is loaded; every call leaves them zero again), and
+ * decode-shaped batches split their keys over several waves only when the
+ * split's partial results fit in the rest (else they run unsplit), so no
+ * batch needs more scratch than the array holds and none is refused for its
+ * size.  Every call on a GPU shares that GPU's array: calls that may overlap
+ * on one GPU (different streams, other threads) race and must not be issued;
+ * calls ordered on one stream are safe.  ILPC_EHIP if the array's address
+ * cannot be looked up on the current device.
+ */
+int ilpc_paged_prefill_attn_noalloc(const uint16_t* q, const uint16_t* k_pool, const uint16_t* v_pool,
+                                    int32_t num_blocks, const int32_t* block_tables, int32_t max_blocks,
+                                    const int32_t* cu_q, const int32_t* seq_lens, int32_t B,
+                                    int32_t max_q_len, int32_t Hq, int32_t Hkv, int32_t D,
+                                    int32_t block_size, float softmax_scale, uint16_t* out, void* stream);
 
 /* Bytes of device workspace ilpc_paged_prefill_attn_cascade needs:
  * 256 + align256(B*max_q_len*Hq*D*4) + align256(B*max_q_len*Hq*8). */

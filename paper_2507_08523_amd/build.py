@@ -18,7 +18,8 @@ LIB = os.path.join(PKG, "libilpc.so")
 SOURCES = [os.path.join(PKG, "csrc", "prefix_cache.cpp"), os.path.join(PKG, "csrc", "pair_table.cpp"),
            os.path.join(PKG, "csrc", "schedule.cpp"),
            os.path.join(PKG, "csrc", "paged_attn.hip"), os.path.join(PKG, "csrc", "rope_append.hip"),
-           os.path.join(PKG, "csrc", "decode_attn.hip")]
+           os.path.join(PKG, "csrc", "decode_attn.hip"),
+           os.path.join(PKG, "csrc", "attn_noalloc.hip")]
 ARCH = "gfx950"
 
 

@@ -41,6 +41,8 @@ _SIGS = [
     ("ilpc_attn_workspace_bytes", _i32, [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)]),
     ("ilpc_paged_prefill_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
                                        _i32, _i32, _i32, _f32, _vp, _vp, ctypes.c_size_t, _vp]),
+    ("ilpc_paged_prefill_attn_noalloc", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
+                                               _i32, _i32, _i32, _f32, _vp, _vp]),
     ("ilpc_paged_decode_attn", _i32, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _i32, _i32, _i32,
                                       _i32, _i32, _i32, _f32, _vp, _i32, _vp, ctypes.c_size_t, _vp]),
     ("ilpc_decode_split", _i32, [_i32, _i32, _i32, ctypes.POINTER(_i32)]),
@@ -431,6 +433,31 @@ def paged_prefill_attn(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_le
             int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3),
             ws_ptr, ws_bytes, _stream(stream))
     _check(load().ilpc_paged_prefill_attn(*args))
+
+
+def paged_prefill_attn_noalloc(q, k_pool, v_pool, block_tables, cu_q, seq_lens, max_q_len: int, scale: float,
+                               out, stream=None):
+    """paged_prefill_attn with the library's static device scratch as its
+    workspace: the call allocates nothing.  Calls that may overlap on one GPU
+    must not be issued (they share that scratch)."""
+    import torch
+
+    NB, Hkv, bs, D = k_pool.shape
+    total, Hq, Dq = q.shape
+    B = cu_q.shape[0] - 1
+    if Dq != D or v_pool.shape != (NB, Hkv, D, bs) or out.shape != q.shape:
+        raise ILPCError(EINVAL, "paged_prefill_attn_noalloc: inconsistent Q/K/V/out shapes")
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ILPCError(EINVAL, "paged_prefill_attn_noalloc: inconsistent batch shapes")
+    args = (_dev(q, torch.bfloat16, "q", 3), _dev(k_pool, torch.bfloat16, "k_pool", 4),
+            _dev(v_pool, torch.bfloat16, "v_pool", 4), NB,
+            _dev(block_tables, torch.int32, "block_tables", 2), block_tables.shape[1],
+            _dev(cu_q, torch.int32, "cu_q", 1), _dev(seq_lens, torch.int32, "seq_lens", 1), B,
+            int(max_q_len), Hq, Hkv, D, bs, float(scale), _dev(out, torch.bfloat16, "out", 3), _stream(stream))
+    _check(load().ilpc_paged_prefill_attn_noalloc(*args))
+
+
+NOALLOC_SCRATCH_BYTES = 256 + (8 << 20)
 
 
 def decode_split(B, Hkv, max_blocks) -> int:
