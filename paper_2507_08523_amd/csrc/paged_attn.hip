@@ -16,8 +16,11 @@
 //    through a 4-tile ring in LDS, filled by direct global-to-LDS loads two
 //    tiles ahead of use.  Per tile and wave:
 //      S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (a lane owns one column),
-//      causal mask, column max, online softmax in fp32 on exp2 with the scale
-//      folded in (O is rescaled only when a column max grows by > 2^8),
+//      causal mask, online softmax in fp32 on exp2 with the scale folded in:
+//      the exponentials are taken against the running column max, and the
+//      tile's column max is computed (and O rescaled) only when a lane's sum
+//      of them leaves [0, 2^8] -- on an item's first tile, or when the max
+//      has grown by several powers of two --,
 //      O^T += V^T P^T on the same MFMA, P taken straight from the S^T
 //      accumulators (K rows are staged in a permuted order that makes the
 //      accumulator layout of S^T equal the operand layout P^T needs).
@@ -167,7 +170,9 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
 // pool block (its K rows and V rows) per tile; the block ids come from the
 // block table through scalar loads, one tile ahead of the load they steer.
 constexpr int kMaxTableBlocks = 1 << 24;  // block-table width accepted (keeps token positions in int)
-constexpr float kLazyRescale = 8.f;  // log2 growth of a column max tolerated before rescaling O
+// Largest per-lane sum of a tile's exponentials accepted without taking the
+// tile's column max (each exponential is then at most this, 2^8).
+constexpr float kSumLimit = 256.f;
 constexpr int kQueueWords = 16;      // workspace: 8 queue counters, 1 finished-workgroup count
 constexpr int kDoneWord = 8;
 
@@ -414,11 +419,17 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     bf16x8 pb[kTileBlocks];    // P of the tile whose V^T P^T is still due
     f32x16 sc0, sc1;           // scores of the tile whose softmax is next
 
-    // Softmax step of the score tile starting at key j0: causal mask, column
-    // max, lazy rescale of O, P = exp2(S * scale_log2 - m), rounded to bf16
-    // for the V^T P^T product while the row sum adds the fp32 values.
+    // Softmax step of the score tile starting at key j0: causal mask, then
+    // P = exp2(S * scale_log2 - m_used), rounded to bf16 for the V^T P^T
+    // product while the row sum adds the fp32 values.  m_used is the column
+    // max the exponentials were last rescaled to.  The step is accepted as
+    // long as every lane's sum of its exponentials lies in [0, 2^8] (so no
+    // single one exceeds 2^8, the headroom the fp32 accumulators are given);
+    // otherwise -- on the first tile (`first`: m_used is still -inf), or when
+    // the max has grown -- the tile's column max is taken, O and the sum are
+    // rescaled to it and the exponentials recomputed.
     // Lane half hh holds keys j0 + (e>>3)*16 + 8*hh + (e&7) [+32] of the tile.
-    auto softmax = [&](int j0) {
+    auto softmax = [&](int j0, bool first) {
       if (MODE != kShared && j0 + kKeys - 1 > wave_pos_min) {  // causal
         const int rel = pos - j0 - hh * 8;  // key (e>>3)*16 + (e&7) [+32] is visible iff <= rel
 #pragma unroll
@@ -448,39 +459,55 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
           sc1[e] = k + 32 < lo ? -INFINITY : sc1[e];
         }
       }
-      // Column max: 16 dependent v_max3_f32 in two asm statements (the
-      // operands come from the matrix cores or are -inf, never signalling
-      // NaNs, so no quieting is needed).  The compiler follows every
-      // inline-asm statement with a wait state, so one statement per
-      // instruction would add 16 of them to the chain.
-      float mx, mx2;
-      asm("v_max3_f32 %0, %1, %2, %3\n\t"
-          "v_max3_f32 %0, %0, %4, %5\n\t"
-          "v_max3_f32 %0, %0, %6, %7\n\t"
-          "v_max3_f32 %0, %0, %8, %9\n\t"
-          "v_max3_f32 %0, %0, %10, %11\n\t"
-          "v_max3_f32 %0, %0, %12, %13\n\t"
-          "v_max3_f32 %0, %0, %14, %15\n\t"
-          "v_max3_f32 %0, %0, %16, %17"
-          : "=&v"(mx)
-          : "v"(sc0[0]), "v"(sc1[0]), "v"(sc0[1]), "v"(sc1[1]), "v"(sc0[2]), "v"(sc1[2]), "v"(sc0[3]),
-            "v"(sc1[3]), "v"(sc0[4]), "v"(sc1[4]), "v"(sc0[5]), "v"(sc1[5]), "v"(sc0[6]), "v"(sc1[6]),
-            "v"(sc0[7]), "v"(sc1[7]), "v"(sc0[8]));
-      asm("v_max3_f32 %0, %1, %2, %3\n\t"
-          "v_max3_f32 %0, %0, %4, %5\n\t"
-          "v_max3_f32 %0, %0, %6, %7\n\t"
-          "v_max3_f32 %0, %0, %8, %9\n\t"
-          "v_max3_f32 %0, %0, %10, %11\n\t"
-          "v_max3_f32 %0, %0, %12, %13\n\t"
-          "v_max3_f32 %0, %0, %14, %15\n\t"
-          "v_max3_f32 %0, %0, %16, %0"
-          : "=&v"(mx2)
-          : "v"(mx), "v"(sc1[8]), "v"(sc0[9]), "v"(sc1[9]), "v"(sc0[10]), "v"(sc1[10]), "v"(sc0[11]),
-            "v"(sc1[11]), "v"(sc0[12]), "v"(sc1[12]), "v"(sc0[13]), "v"(sc1[13]), "v"(sc0[14]),
-            "v"(sc1[14]), "v"(sc0[15]), "v"(sc1[15]));
-      mx = mx2;
-      mx = max_across_halves(mx) * scale_log2;
-      if (__ballot(mx > m_used + kLazyRescale)) {
+      // Exponentials against the running max m_used, summed per lane half.
+      auto exps = [&](float* ls) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc0[e], scale_log2, -m_used));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc1[e], scale_log2, -m_used));
+          pb[e >> 3][e & 7] = (__bf16)p0;
+          pb[2 + (e >> 3)][e & 7] = (__bf16)p1;
+          ls[e & 3] += p0 + p1;
+        }
+      };
+      float ls[4] = {0.f, 0.f, 0.f, 0.f};
+      float tsum = 0.f;
+      bool slow = first;
+      if (!first) {
+        exps(ls);
+        tsum = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+        // Accepted unless some lane's sum exceeds kSumLimit or is not a
+        // number (an overflow, or -inf - -inf).
+        slow = __ballot(!(tsum <= kSumLimit)) != 0;
+      }
+      if (slow) {
+        float mx, mx2;
+        asm("v_max3_f32 %0, %1, %2, %3\n\t"
+            "v_max3_f32 %0, %0, %4, %5\n\t"
+            "v_max3_f32 %0, %0, %6, %7\n\t"
+            "v_max3_f32 %0, %0, %8, %9\n\t"
+            "v_max3_f32 %0, %0, %10, %11\n\t"
+            "v_max3_f32 %0, %0, %12, %13\n\t"
+            "v_max3_f32 %0, %0, %14, %15\n\t"
+            "v_max3_f32 %0, %0, %16, %17"
+            : "=&v"(mx)
+            : "v"(sc0[0]), "v"(sc1[0]), "v"(sc0[1]), "v"(sc1[1]), "v"(sc0[2]), "v"(sc1[2]), "v"(sc0[3]),
+              "v"(sc1[3]), "v"(sc0[4]), "v"(sc1[4]), "v"(sc0[5]), "v"(sc1[5]), "v"(sc0[6]), "v"(sc1[6]),
+              "v"(sc0[7]), "v"(sc1[7]), "v"(sc0[8]));
+        asm("v_max3_f32 %0, %1, %2, %3\n\t"
+            "v_max3_f32 %0, %0, %4, %5\n\t"
+            "v_max3_f32 %0, %0, %6, %7\n\t"
+            "v_max3_f32 %0, %0, %8, %9\n\t"
+            "v_max3_f32 %0, %0, %10, %11\n\t"
+            "v_max3_f32 %0, %0, %12, %13\n\t"
+            "v_max3_f32 %0, %0, %14, %15\n\t"
+            "v_max3_f32 %0, %0, %16, %0"
+            : "=&v"(mx2)
+            : "v"(mx), "v"(sc1[8]), "v"(sc0[9]), "v"(sc1[9]), "v"(sc0[10]), "v"(sc1[10]), "v"(sc0[11]),
+              "v"(sc1[11]), "v"(sc0[12]), "v"(sc1[12]), "v"(sc0[13]), "v"(sc1[13]), "v"(sc0[14]),
+              "v"(sc1[14]), "v"(sc0[15]), "v"(sc1[15]));
+        mx = mx2;
+        mx = max_across_halves(mx) * scale_log2;
         const float m_new = fmaxf(m_used, mx);
         const float alpha = __builtin_amdgcn_exp2f(m_used - m_new);
         m_used = m_new;
@@ -489,17 +516,11 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
         for (int dt = 0; dt < kDt; ++dt)
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+        ls[0] = ls[1] = ls[2] = ls[3] = 0.f;
+        exps(ls);
+        tsum = (ls[0] + ls[1]) + (ls[2] + ls[3]);
       }
-      float ls[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc0[e], scale_log2, -m_used));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc1[e], scale_log2, -m_used));
-        pb[e >> 3][e & 7] = (__bf16)p0;
-        pb[2 + (e >> 3)][e & 7] = (__bf16)p1;
-        ls[e & 3] += p0 + p1;
-      }
-      l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      l_run += tsum;
     };
 
     // One matrix-core phase: O += V(sV) P over the tile's pool blocks
@@ -615,7 +636,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     if (n_tiles > 1) wait_tile(1);
     bare_barrier();
     prefetch_id(0);
-    if (0 <= wave_last) softmax(t0 * kKeys);
+    if (0 <= wave_last) softmax(t0 * kKeys, MODE != kSuffix);
     for (int j = 1; j < n_tiles; ++j) {
       begin_m(j);
       // Tiles past the wave's last visible key are skipped; the step right
@@ -624,7 +645,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
       if (j + 1 < n_tiles) wait_tile(j + 1);
       bare_barrier();
       prefetch_id(j);
-      if (j <= wave_last) softmax((t0 + j) * kKeys);
+      if (j <= wave_last) softmax((t0 + j) * kKeys, false);
     }
     begin_m(n_tiles);
     if (n_tiles - 1 <= wave_last) m_phase(yes(), no(), stage(n_tiles - 1) + kKTileBytes, stage(0));
