@@ -362,11 +362,19 @@ int ilpc_attn_cascade_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, 
  * The same attention as ilpc_paged_prefill_attn, split at a prefix that every
  * request of the batch shares (the instruction and leading demonstrations of
  * the log-parsing prompts, section 2.1.1, which prefix caching stores once,
- * section 2.1.2): first every query row of the batch attends to the shared
- * keys 0 .. shared_len-1 in one pass (their K/V is read once per 256 query
- * columns of the whole batch, not once per request), then each request's
- * queries attend to their own keys shared_len .. L_r-1 starting from that
- * state, and the two halves are merged exactly (online-softmax rescaling).
+ * section 2.1.2): the shared keys are read once per 256 query columns of the
+ * whole batch (query row x q head of a kv head), not once per request.
+ *   - Prefill-shaped batches (max_q_len * Hq / Hkv >= 64) whose shared prefix
+ *     holds at least three 64-key tiles, and whose per-item tile list fits
+ *     ((256 / G + 1) * (ceil(16 * max_blocks / 64) - floor(shared_len / 64))
+ *     <= 2048, G = Hq / Hkv), run as one launch: each workgroup takes 256
+ *     columns of the batch, attends them to the floor(shared_len / 64) * 64
+ *     shared keys, then to each of their requests' own keys from there on
+ *     (masked to that request's columns, causal), in one online softmax.
+ *   - Other batches (decode steps among them) run two launches: every query
+ *     row over keys 0 .. shared_len-1, with the unnormalised state in the
+ *     workspace, then each request's queries over its keys shared_len ..
+ *     L_r-1, continuing from that state.
  *
  * shared_len  [host] a multiple of 16 in [0, 16*max_blocks].  The caller
  *             guarantees that the first shared_len/16 entries of every
@@ -376,7 +384,8 @@ int ilpc_attn_cascade_workspace_bytes(int32_t B, int32_t max_q_len, int32_t Hq, 
  * workspace   [device] >= ilpc_attn_cascade_workspace_bytes() bytes,
  *             16-byte aligned, its first 128 bytes zero-filled before the
  *             first use (each call leaves them zero-filled again); the rest
- *             holds fp32 partial results, overwritten by every call.
+ *             holds fp32 partial results of the two-launch form,
+ *             overwritten by every such call.
  * Other arguments and the result as for ilpc_paged_prefill_attn; rows of
  * requests whose q_len exceeds max_q_len are not computed.  If the
  * shared_len contract does not hold the output is unspecified, but no

@@ -26,10 +26,15 @@
 //      accumulator layout of S^T equal the operand layout P^T needs).
 //    The two waves sharing a SIMD run these steps half a tile apart, so one
 //    feeds the matrix core while the other computes the softmax.
+//  * the same attention split at a prefix every request of the batch shares
+//    (modes kShared / kSuffix: two launches; kFused: one launch whose items
+//    are 256 columns of the whole batch, over the shared tiles and then each
+//    of their requests' own tiles).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
+#include <climits>
 #include <cstdint>
 #include <type_traits>
 
@@ -213,7 +218,16 @@ __device__ __forceinline__ unsigned xcd_id() {
 // Splitting this way reads the shared K/V once per column tile of the whole
 // batch instead of once per request (the log-sum-exp merge of the two halves
 // is exact up to rounding).
-enum AttnMode { kFull = 0, kShared = 1, kSuffix = 2 };
+//   kFused:  the same split in one launch: every item is 256 columns of the
+//            whole batch's packed query rows (like kShared); it runs the
+//            kv_split / 64 tiles every request shares, then, for each
+//            request its rows belong to, that request's own tiles from
+//            kv_split on, masked to that request's columns.  No partial
+//            state leaves the workgroup.
+enum AttnMode { kFull = 0, kShared = 1, kSuffix = 2, kFused = 3 };
+
+// kFused: per item, the request tiles after the shared ones, in LDS.
+constexpr int kFusedTiles = 2048;
 
 template <int D, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
@@ -239,6 +253,11 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   static_assert(kStages == 4, "ring: two tiles in flight plus two being read");
   __shared__ __attribute__((aligned(16))) uint8_t ring[kStages * kStageBytes];
   __shared__ int s_item[2];
+  // kFused: tile T_s + i of an item is tile f_tt[i] of request r_a + f_rel[i],
+  // whose keys at or past f_lim[i] no row of the item sees.
+  constexpr int kFT = MODE == kFused ? kFusedTiles : 1;
+  __shared__ int f_rel[kFT], f_tt[kFT], f_lim[kFT];
+  __shared__ int f_count;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -294,10 +313,13 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   for (int it = 0;; ++it) {
     const int w = __builtin_amdgcn_readfirstlane(s_item[it & 1]);
     if (w < 0) break;
-    const int tile = n_col_tiles - 1 - int(unsigned(w) % unsigned(n_col_tiles));
+    // kFused numbers items kv-head-major (the items of one kv head share the
+    // prefix blocks, under one XCD's L2).
+    const int tile = MODE == kFused ? int(unsigned(w) % unsigned(n_col_tiles))
+                                    : n_col_tiles - 1 - int(unsigned(w) % unsigned(n_col_tiles));
     const unsigned rest = unsigned(w) / unsigned(n_col_tiles);
-    const int kvh = int(rest % unsigned(Hkv));
-    const int r = MODE == kShared ? 0 : int(rest / unsigned(Hkv));
+    const int kvh = MODE == kFused ? int(rest) : int(rest % unsigned(Hkv));
+    const int r = MODE == kShared || MODE == kFused ? 0 : int(rest / unsigned(Hkv));
     // First key tile of this launch (the suffix half starts at kv_split).
     const int t0 = MODE == kSuffix ? kv_split / kKeys : 0;
     // This item's lengths and the block ids of its first three tiles are
@@ -306,21 +328,31 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     // used, so that no wait follows the scalar load.
     const int32_t* bt = block_tables + size_t(r) * max_blocks;
     auto raw_id = [&](int tl) { return bt[min((t0 + tl) * kTileBlocks + my_blk, max_blocks - 1)]; };
+    // kFused: request (relative to r_a) and tile of item tile tl.
+    auto fused_src = [&](int tl, int& rel, int& tt) {
+      if (tl < kv_split / kKeys) {
+        rel = 0;
+        tt = tl;
+      } else {
+        rel = __builtin_amdgcn_readfirstlane(f_rel[tl - kv_split / kKeys]);
+        tt = __builtin_amdgcn_readfirstlane(f_tt[tl - kv_split / kKeys]);
+      }
+    };
     // The shared half treats the whole batch as one request whose queries all
     // follow the kv_split shared keys.
-    const int q0 = MODE == kShared ? 0 : cu_q[r];
-    const int q_end = MODE == kShared ? cu_q[n_req] : cu_q[r + 1];
-    const int L_in = MODE == kShared ? kv_split + (q_end - q0) : seq_lens[r];
+    const int q0 = MODE == kShared || MODE == kFused ? 0 : cu_q[r];
+    const int q_end = MODE == kShared || MODE == kFused ? cu_q[n_req] : cu_q[r + 1];
+    const int L_in = MODE == kShared || MODE == kFused ? kv_split + (q_end - q0) : seq_lens[r];
     const int raw_id0 = raw_id(0), raw_id1 = raw_id(1);
     int raw_next = raw_id(2);  // raw id of the next tile to issue after tile 1
     // First use of all six values at once: the loads are issued together and
     // waited for once.
     asm volatile("" : : "s"(q0), "s"(q_end), "s"(L_in), "s"(raw_id0), "s"(raw_id1), "s"(raw_next));
     // In the split modes, rows past the partial-state buffer are not computed.
-    const int q_len = MODE == kFull ? q_end - q0 : min(q_end, part_rows) - q0;
+    const int q_len = MODE == kFull || MODE == kFused ? q_end - q0 : min(q_end, part_rows) - q0;
     const int n_cols = q_len * G;
     const int col0 = tile * kCols;
-    const int L = MODE == kShared ? L_in : min(L_in, max_blocks * kBlock);
+    const int L = MODE == kShared || MODE == kFused ? L_in : min(L_in, max_blocks * kBlock);
     if (q_len <= 0 || col0 >= n_cols || q_len > L) {  // nothing to do for this item
       if (tid == 0) {
         s_item[(it + 1) & 1] = fetch();
@@ -331,6 +363,8 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     }
     const int qstart = L - q_len;  // position of the request's first query
 
+    const int T_s = kv_split / kKeys;  // kFused: tiles every request shares (at least 3)
+    int r_a = 0, my_rel = 0, my_pos = 0;
     // This lane's query column (padding columns repeat the last valid one).
     const int col = col0 + wave * kColsPerWave + n;
     const bool col_valid = col < n_cols;
@@ -345,18 +379,28 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const int wg_pos_max = qstart + min(col0 + kCols - 1, n_cols - 1) / G;
     // Keys at or past key_lim are masked everywhere (and their V rows zeroed).
     const int key_lim = MODE == kShared ? kv_split : wg_pos_max + 1;
-    const int n_tiles = (key_lim - 1) / kKeys + 1 - t0;  // tiles of this launch, from t0
+    // Tiles of this launch (kFused: the shared ones until the item's list is
+    // read after the first barrier).
+    int n_tiles = MODE == kFused ? T_s : (key_lim - 1) / kKeys + 1 - t0;
     const int n_blk_used = (key_lim + kBlock - 1) / kBlock;  // <= ceil(L / 16) <= max_blocks
     // Last tile (counted from t0) holding a key some column of this wave sees
     // (-1: no column).
-    const int wave_last =
+    int wave_last =
         !wave_active ? -1
-        : MODE == kShared ? n_tiles - 1
+        : MODE == kShared || MODE == kFused ? n_tiles - 1
                           : (qstart + min(wave_first + kColsPerWave - 1, n_cols - 1) / G) / kKeys - t0;
 
     bf16x8 qf[kDch];
 #pragma unroll
     for (int kc = 0; kc < kDch; ++kc) qf[kc] = as_bf16x8(*(const u32x4*)(q + qrow + kc * 16 + hh * 8));
+    // kFused: block id of this wave in item tile tl (shared tiles from any
+    // request's table, request tiles from the owner's).
+    auto fused_raw = [&](int tl) {
+      int rel, tt;
+      fused_src(tl, rel, tt);
+      return block_tables[size_t(r_a + rel) * max_blocks + min(tt * kTileBlocks + my_blk, max_blocks - 1)];
+    };
+
 
     const uint8_t* kbase = reinterpret_cast<const uint8_t*>(k_pool) + size_t(kvh) * kSlabBytes;
     const uint8_t* vbase = reinterpret_cast<const uint8_t*>(v_pool) + size_t(kvh) * kSlabBytes;
@@ -364,6 +408,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     // ids read block 0 instead (stray K rows only meet masked scores, stray V
     // rows past key_lim are zeroed below).
     auto usable = [&](int tl, int id) {
+      if constexpr (MODE == kFused) return (id >= 0 && id < num_blocks) ? id : 0;
       return ((t0 + tl) * kTileBlocks + my_blk < n_blk_used && id >= 0 && id < num_blocks) ? id : 0;
     };
     auto stage = [&](int tl) { return ring + (unsigned(tbase + tl) % unsigned(kStages)) * kStageBytes; };
@@ -379,7 +424,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
         global_to_lds16(vsrc + voff[i], st + kKTileBytes + (wave * kVInsts + i) * 1024);
     };
     // Zero the V rows of keys >= key_lim in a V tile (only the tile crossing it).
-    auto zero_v_tail = [&](int j0, uint8_t* sV) {
+    auto zero_v_tail = [&](int j0, uint8_t* sV, int key_lim) {
       for (int slot = tid; slot < kVTileBytes / 16; slot += kThreads) {
         const int kb = slot / (2 * D), d = (slot % (2 * D)) >> 1, p = slot & 1;
         const int nvalid = key_lim - (j0 + kb * kBlock + v_slot(d, p) * 8);
@@ -429,8 +474,17 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     // the max has grown -- the tile's column max is taken, O and the sum are
     // rescaled to it and the exponentials recomputed.
     // Lane half hh holds keys j0 + (e>>3)*16 + 8*hh + (e&7) [+32] of the tile.
-    auto softmax = [&](int j0, bool first) {
-      if (MODE != kShared && j0 + kKeys - 1 > wave_pos_min) {  // causal
+    auto softmax = [&](int j0, bool first, int fused_thr) __attribute__((always_inline)) {
+      if (MODE == kFused && fused_thr != INT_MAX) {  // a request tile: its own rows, causal
+        const int rel = fused_thr;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int k = (e >> 3) * 16 + (e & 7);
+          sc0[e] = k > rel ? -INFINITY : sc0[e];
+          sc1[e] = k + 32 > rel ? -INFINITY : sc1[e];
+        }
+      }
+      if (MODE != kShared && MODE != kFused && j0 + kKeys - 1 > wave_pos_min) {  // causal
         const int rel = pos - j0 - hh * 8;  // key (e>>3)*16 + (e&7) [+32] is visible iff <= rel
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -467,10 +521,13 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
           const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc1[e], scale_log2, -m_used));
           pb[e >> 3][e & 7] = (__bf16)p0;
           pb[2 + (e >> 3)][e & 7] = (__bf16)p1;
-          ls[e & 3] += p0 + p1;
+          ls[e & 3] = e < 4 ? p0 + p1 : ls[e & 3] + (p0 + p1);
         }
+        // The bf16 operands are formed here, not after the acceptance test:
+        // sunk past it, all 32 fp32 exponentials would stay live across it.
+        asm volatile("" : "+v"(pb[0]), "+v"(pb[1]), "+v"(pb[2]), "+v"(pb[3]));
       };
-      float ls[4] = {0.f, 0.f, 0.f, 0.f};
+      float ls[4];
       float tsum = 0.f;
       bool slow = first;
       if (!first) {
@@ -516,7 +573,6 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
         for (int dt = 0; dt < kDt; ++dt)
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
-        ls[0] = ls[1] = ls[2] = ls[3] = 0.f;
         exps(ls);
         tsum = (ls[0] + ls[1]) + (ls[2] + ls[3]);
       }
@@ -608,8 +664,19 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     };
     auto begin_m = [&](int j) {
       bare_barrier();
-      if (j < n_tiles && (t0 + j) * kKeys + kKeys > key_lim) {
-        zero_v_tail((t0 + j) * kKeys, stage(j) + kKTileBytes);
+      if (MODE == kFused && j == 0) {  // the item's list is complete (wave 0 waited before this barrier)
+        n_tiles = T_s + __builtin_amdgcn_readfirstlane(f_count);
+        wave_last = wave_active ? n_tiles - 1 : -1;
+      }
+      if (MODE == kFused && j >= T_s && j < n_tiles) {
+        const int i = j - T_s;
+        const int tt = __builtin_amdgcn_readfirstlane(f_tt[i]), lim = __builtin_amdgcn_readfirstlane(f_lim[i]);
+        if (tt * kKeys + kKeys > lim) {
+          zero_v_tail(tt * kKeys, stage(j) + kKTileBytes, lim);
+          wait_lgkmcnt0();
+        }
+      } else if (MODE != kFused && j < n_tiles && (t0 + j) * kKeys + kKeys > key_lim) {
+        zero_v_tail((t0 + j) * kKeys, stage(j) + kKTileBytes, key_lim);
         wait_lgkmcnt0();  // zeros in LDS before the next barrier
       }
       if (j + 2 < n_tiles) issue_tile(j + 2, raw_next);
@@ -618,11 +685,57 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     // read follows until the next phase, so the scalar load (which shares
     // lgkmcnt with LDS reads) has landed before anything waits on lgkmcnt.
     auto prefetch_id = [&](int j) {
-      if (j + 3 < n_tiles) raw_next = raw_id(j + 3);
+      if (j + 3 < n_tiles) raw_next = MODE == kFused ? fused_raw(j + 3) : raw_id(j + 3);
     };
 
     issue_tile(0, raw_id0);
     if (1 < n_tiles) issue_tile(1, raw_id1);
+    // kFused: with the first tiles and Q in flight, find the requests of the
+    // item's rows, this lane's request and position, and (wave 0) the list of
+    // request tiles; tiles 0-2 are shared, so request 0's table gave their ids.
+    // Scalar loads only: they do not queue behind the tiles' vector loads.
+    if constexpr (MODE == kFused) {
+      const int row_a = col0 / G, row_b = min(col0 + kCols - 1, n_cols - 1) / G;
+      // r_a: the largest request whose first row is at or before row_a
+      int lo = 0, hi = n_req;  // cu_q[lo] <= row_a < cu_q[hi]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (cu_q[mid] <= row_a) lo = mid;
+        else hi = mid;
+      }
+      r_a = lo;
+      const int col_l = min(col0 + wave * kColsPerWave + n, n_cols - 1);
+      const int row_l = col_l / G;
+      int n_list = 0;
+      // requests r_a, r_a + 1, ... while their rows start at or before row_b
+      for (int rr = r_a; rr < n_req; ++rr) {
+        const int b0 = cu_q[rr];
+        if (b0 > row_b) break;
+        const int b1 = cu_q[rr + 1];
+        const int lo_row = max(b0, row_a), hi_row = min(b1 - 1, row_b);
+        if (lo_row > hi_row) continue;  // no row of this item (or an empty request)
+        const int Lr = min(seq_lens[rr], max_blocks * kBlock);
+        if (row_l >= b0 && row_l < b1) {
+          my_rel = rr - r_a;
+          my_pos = Lr - (b1 - b0) + (row_l - b0);
+        }
+        // keys the item's rows of rr see end at lim; its tiles T_s .. go to the list
+        const int lim = Lr - (b1 - b0) + (hi_row - b0) + 1;
+        const int cnt = min(max(0, (lim + kKeys - 1) / kKeys - T_s), kFusedTiles - n_list);
+        if (wave == 0) {
+          for (int k = lane; k < cnt; k += 64) {
+            f_rel[n_list + k] = rr - r_a;
+            f_tt[n_list + k] = T_s + k;
+            f_lim[n_list + k] = lim;
+          }
+        }
+        n_list += cnt;
+      }
+      if (wave == 0) {
+        if (lane == 0) f_count = n_list;
+        wait_lgkmcnt0();  // the list is in LDS before the barrier that opens M_0
+      }
+    }
     if (tid == 0) {  // the next item, fetched while the first tiles load
       s_item[(it + 1) & 1] = fetch();
       wait_lgkmcnt0();
@@ -631,12 +744,32 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     // stands in for the barrier opening V_{-1}).
     wait_vmcnt<0>();
     if (lag) bare_barrier();
+    // kFused: mask threshold of item tile j for this lane (INT_MAX: a shared
+    // tile, all keys visible) and the tile's first key in its request.
+    auto fused_thr = [&](int j, int& j0) {
+      if (j < T_s) {
+        j0 = j * kKeys;
+        return INT_MAX;
+      }
+      const int rel = __builtin_amdgcn_readfirstlane(f_rel[j - T_s]);
+      j0 = __builtin_amdgcn_readfirstlane(f_tt[j - T_s]) * kKeys;
+      return rel == my_rel ? my_pos - j0 - hh * 8 : -1;
+    };
+    auto soft = [&](int j, bool first) __attribute__((always_inline)) {
+      if constexpr (MODE == kFused) {
+        int j0;
+        const int th = fused_thr(j, j0);
+        softmax(j0, first, th);
+      } else {
+        softmax((t0 + j) * kKeys, first, INT_MAX);
+      }
+    };
     begin_m(0);
     if (0 <= wave_last) m_phase(no(), yes(), stage(0), stage(0));
     if (n_tiles > 1) wait_tile(1);
     bare_barrier();
     prefetch_id(0);
-    if (0 <= wave_last) softmax(t0 * kKeys, MODE != kSuffix);
+    if (0 <= wave_last) soft(0, MODE != kSuffix);
     for (int j = 1; j < n_tiles; ++j) {
       begin_m(j);
       // Tiles past the wave's last visible key are skipped; the step right
@@ -645,7 +778,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
       if (j + 1 < n_tiles) wait_tile(j + 1);
       bare_barrier();
       prefetch_id(j);
-      if (j <= wave_last) softmax((t0 + j) * kKeys, false);
+      if (j <= wave_last) soft(j, false);
     }
     begin_m(n_tiles);
     if (n_tiles - 1 <= wave_last) m_phase(yes(), no(), stage(n_tiles - 1) + kKTileBytes, stage(0));
@@ -834,7 +967,7 @@ int launch_attn(const char* fn, const uint16_t* q, const uint16_t* k_pool, const
                 const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int64_t col_tiles,
                 float scale_log2, uint16_t* out, unsigned* queue, int kv_split, float* part_o,
                 float* part_ml, int part_rows, hipStream_t s) {
-  const int64_t items = col_tiles * Hkv * (MODE == kShared ? 1 : B);
+  const int64_t items = col_tiles * Hkv * (MODE == kShared || MODE == kFused ? 1 : B);
   if (items == 0) return ILPC_OK;
   const int cus = device_cus();
   if (cus <= 0) return ilpc::set_error(ILPC_EHIP, "%s: cannot query the device", fn);
@@ -973,6 +1106,17 @@ extern "C" int ilpc_paged_prefill_attn_cascade(
     return launch_attn<kFull>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens,
                               B, Hq, Hkv, D, col_tiles, scale_log2, out, queue_shared, 0, nullptr, nullptr,
                               0, s);
+  // One launch (kFused) for prefill-shaped batches whose shared prefix holds
+  // at least three 64-key tiles and whose per-item tile list fits: at most
+  // 256 / G + 1 requests have rows in an item, each with at most
+  // ceil(16 * max_blocks / 64) - T_s tiles of its own.
+  const int64_t T_s = shared_len / kKeys;
+  const int64_t own_tiles = std::max<int64_t>(0, (int64_t(max_blocks) * kBlock + kKeys - 1) / kKeys - T_s);
+  if (T_s >= 3 && int64_t(max_q_len) * G >= 2 * kColsPerWave &&
+      ((kCols + G - 1) / G + 1) * own_tiles <= kFusedTiles)
+    return launch_attn<kFused>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
+                               Hq, Hkv, D, (rows * G + kCols - 1) / kCols, scale_log2, out, queue_shared,
+                               int(T_s * kKeys), nullptr, nullptr, int(rows), s);
   rc = launch_attn<kShared>(fn, q, k_pool, v_pool, num_blocks, block_tables, max_blocks, cu_q, seq_lens, B,
                             Hq, Hkv, D, (rows * G + kCols - 1) / kCols, scale_log2, out, queue_shared,
                             shared_len, part_o, part_ml, int(rows), s);

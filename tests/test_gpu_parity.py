@@ -507,3 +507,55 @@ def test_cascade_decode_steps_against_oracle():
             worst = max(worst, float(err.max()))
             assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, (s, r)
     log(f"[parity] sweep100 decode (cascade): {wl.spec.decode_steps} steps, max_abs={worst:.3e}")
+
+
+@pytest.mark.parametrize("q_pattern", ["ragged", "small", "with_empty"])
+def test_cascade_fused_many_requests_per_item(q_pattern):
+    # Prefill-shaped cascades with at least three shared 64-key tiles run as
+    # one launch whose items are 256 columns of the whole batch: here each
+    # request keeps only its last k queries (k ragged, small so that one item
+    # spans up to 64 requests, or zero for some requests), so items mix many
+    # requests and request tiles are masked to their own columns.
+    from paper_2507_08523_amd.pipeline import shared_prefix_len
+
+    run = Run(workload.scaled_spec("sweep100", 40))
+    wl, pc, sp = run.wl, run.pc, run.wl.spec
+    B = len(wl.prompts)
+    L = wl.seq_lens.astype(np.int64)
+    S = L - run.cached
+    rng = np.random.default_rng({"ragged": 1, "small": 2, "with_empty": 3}[q_pattern])
+    if q_pattern == "ragged":
+        k = rng.integers(1, S + 1)
+    elif q_pattern == "small":
+        k = rng.integers(1, 17, B)
+        k[0] = 16  # max_q_len * G = 64: still prefill-shaped, so the one-launch split
+    else:
+        k = np.where(rng.random(B) < 0.3, 0, rng.integers(1, S + 1))
+    k = np.minimum(k, S).astype(np.int64)
+    cu = np.zeros(B + 1, np.int64)
+    cu[1:] = np.cumsum(k)
+    rows = wl.packed_rows([(r, int(L[r] - k[r]), int(L[r])) for r in range(B)])
+    q = rows["q"]
+    b = pc.upload(run.tables, cu.astype(np.int32), L.astype(np.int32), (L - k).astype(np.int32))
+    sl = shared_prefix_len(run.cached, run.tables)
+    assert sl == 976
+    ws = pc.cascade_workspace(b, sp.n_q_heads)
+    out = torch.full_like(q, float("nan"))
+    pc.attend_cascade(b, q, out, sp.scale, sl, ws)
+    torch.cuda.synchronize()
+    worst, tot, cnt = 0.0, 0.0, 0
+    for r in range(B):
+        if k[r] == 0:
+            continue
+        kk, vv = wl.dense_kv(r, int(L[r]))
+        ref = prefill_attention_ref(wl.q_rows(r, int(L[r] - k[r]), int(L[r])).float().cpu().numpy(),
+                                    kk.float().cpu().numpy(), vv.float().cpu().numpy(), sp.scale)
+        got = out[int(cu[r]):int(cu[r + 1])].float().cpu().numpy()
+        assert np.isfinite(got).all(), r
+        err = np.abs(got - ref)
+        worst = max(worst, float(err.max()))
+        tot += float(err.sum())
+        cnt += err.size
+    log(f"[parity] sweep100[40] cascade, {q_pattern} queries ({int(k.sum())} rows, {int((k == 0).sum())} "
+        f"empty requests): max_abs={worst:.3e} mean_abs={tot / cnt:.3e}")
+    assert worst <= MAX_ABS and tot / cnt <= MEAN_ABS
