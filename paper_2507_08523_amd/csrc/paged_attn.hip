@@ -595,6 +595,15 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
         const int u = st - kPvSteps, m = (u & 1) * 32 + n;
         return *(const bf16x8*)(sK + m * kRowBytes + (k_slot<D>(m, (u >> 1) * 2 + hh) << 4));
       };
+      // Raised issue priority for the phase: when the partner wave's softmax
+      // and this wave's next product are both ready, the product goes first,
+      // so the matrix core does not wait behind a run of vector instructions
+      // (1-2.5% faster than equal priority on llama8b, qwen7b, large and
+      // sweep100).  The scheduling barriers keep the phase's instructions
+      // between the two priority changes.
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(1);
+      __builtin_amdgcn_sched_barrier(0);
       if constexpr (decltype(with_qk)::value) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) { sc0[e] = 0.f; sc1[e] = 0.f; }
@@ -626,6 +635,9 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_group_barrier(0x008, lead, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_sched_barrier(0);
     };
     using yes = std::true_type;
     using no = std::false_type;
