@@ -104,8 +104,17 @@ def workload_work(wl, cached_len, tables):
 
 
 def kernel_source_sha() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the attention kernel's code: `//` comments, trailing blanks and
+    empty lines are left out, so a comment edit does not orphan the counter
+    summaries taken on the same code (the source has no block comments and
+    no `//` inside string literals)."""
+    lines = []
+    with open(KERNEL_SRC, encoding="utf-8") as f:
+        for line in f:
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                lines.append(code)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()[:16]
 
 
 def traffic_from_profile(workload_name: str):

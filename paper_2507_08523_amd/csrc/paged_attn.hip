@@ -13,8 +13,8 @@
 //    (token, q head of the group) pair, so the G heads of a group share every
 //    K/V tile.  The kernel is persistent (one 8-wave workgroup per CU) and
 //    takes items from per-XCD queues.  64-key tiles (4 pool blocks) stream
-//    through a 4-tile ring in LDS, filled by direct global-to-LDS loads two
-//    tiles ahead of use.  Per tile and wave:
+//    through a 4-tile ring in LDS, filled by direct global-to-LDS loads
+//    issued a tile step ahead of use.  Per tile and wave:
 //      S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (a lane owns one column),
 //      causal mask, online softmax in fp32 on exp2 with the scale folded in:
 //      the exponentials are taken against the running column max, and the
@@ -171,7 +171,8 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
 // the caller's workspace; the last workgroup to finish clears them again.
 //
 // K/V tiles stream through a ring of kStages tiles in LDS, filled straight
-// from HBM by global_load_lds two tiles ahead of use.  Each wave loads one
+// from HBM by global_load_lds (tile j+2 issued while tile j's softmax runs).
+// Each wave loads one
 // pool block (its K rows and V rows) per tile; the block ids come from the
 // block table through scalar loads, one tile ahead of the load they steer.
 constexpr int kMaxTableBlocks = 1 << 24;  // block-table width accepted (keeps token positions in int)

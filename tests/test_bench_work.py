@@ -72,3 +72,18 @@ def test_sweep100_unique_bytes_count_the_shared_prefix_once(lib):
     assert w["logical_bytes"] == kv_tok * 128 * 1024 + qo
     assert w["unique_bytes"] == kv_tok * (976 + 128 * 48) + qo
     assert abs(w["unique_bytes"] / 1e6 - 130) < 1 and abs(w["logical_bytes"] / 1e6 - 638) < 1
+
+
+def test_kernel_hash_ignores_comments_only(tmp_path, monkeypatch):
+    # the counter summaries are keyed on the kernel's code: a comment edit
+    # keeps the hash, a code edit changes it
+    import bench
+
+    src = tmp_path / "k.hip"
+    src.write_text("int f(int x) {  // doubles\n  return 2 * x;\n}\n")
+    monkeypatch.setattr(bench, "KERNEL_SRC", str(src))
+    h0 = bench.kernel_source_sha()
+    src.write_text("// a new header line\nint f(int x) {  // twice x\n\n  return 2 * x;   \n}\n")
+    assert bench.kernel_source_sha() == h0
+    src.write_text("int f(int x) {\n  return 3 * x;\n}\n")
+    assert bench.kernel_source_sha() != h0
