@@ -8,8 +8,8 @@
  *     (section 2.1.1, prompt format);
  *   - KV of a shared prompt prefix is reused across requests at block
  *     granularity, and a block is reusable only if every block before it is
- *     reused too (section 2.1.2, "KV Cache and Prefix Caching", and its
- *     three-request figure);
+ *     reused too (section 2.1.2 on the KV cache and prefix caching, and
+ *     its three-request figure);
  *   - the KV of cache-missing tokens is computed and stored (section 3.2.2);
  *   - prefill over the uncached suffix against cached + new KV dominates the
  *     latency (section 2.2.1).
@@ -442,9 +442,9 @@ int ilpc_shared_prefix_len(const int32_t* cached_len, const int32_t* block_table
                            int32_t max_blocks, int32_t* shared_len);
 
 /*
- * Prefix-aware refinement of in-context demonstrations (section 3.2.1,
- * "Prefix-Aware ICL Refinement", with its matching / modifying / reordering
- * figure, and section 3.2.2, "ICL Table Management").  Host only,
+ * Prefix-aware refinement of in-context demonstrations (section 3.2.1, with
+ * its matching / modifying / reordering figure, and section 3.2.2 on the ICL
+ * table).  Host only,
  * synchronous; the table is library-owned host memory.
  *
  * A demonstration is a (template id, demonstration id) pair of int32 values:
