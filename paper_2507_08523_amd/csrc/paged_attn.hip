@@ -819,6 +819,50 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
               *(f32x4*)(part_o + prow * D + dt * 32 + g4 * 8 + hh * 4) = v;
             }
         }
+      } else if constexpr (D == 128) {
+        // The normalised O leaves through LDS.  In the matrix-core layout a
+        // lane holds 8-byte pieces of one output row, so direct stores put 16
+        // bytes of 32 different rows into every instruction; those scattered
+        // stores held up the item boundary (timed without them, llama8b and
+        // large ran 16% and 8% faster).  Each wave writes its 32 rows, 64
+        // dimensions at a time, into its 4 KiB of the ring stage the next
+        // item's tile 2 will take, then stores whole 128-byte half rows, 8
+        // lanes per half row.  That stage (tile n-2's) is free: its last
+        // reader M_{n-1} ended by barrier 2n everywhere, and the next item
+        // writes it only in its V_0, after both halves have passed here.
+        // 16-byte chunks are XOR-swizzled by row against bank conflicts.
+        const float inv = 1.f / l_tot;
+        uint8_t* tb = stage(2) + wave * (kStageBytes / kWaves);
+        static_assert(kStageBytes / kWaves >= kColsPerWave * 128, "transpose area");
+        size_t orow4[4];  // output row of the 4 rows this lane stores
+        bool ok4[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int c = col0 + wave * kColsPerWave + r * 8 + (lane >> 3);
+          ok4[r] = c < n_cols;
+          const int tr = c / G;
+          orow4[r] = (size_t(q0 + tr) * Hq + size_t(kvh) * G + (c - tr * G)) * D;
+        }
+        const int ch_r = lane & 7;
+#pragma unroll
+        for (int p = 0; p < kDt / 2; ++p) {
+#pragma unroll
+          for (int dl = 0; dl < 2; ++dl)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+              bf16x4 v;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = (__bf16)(o[2 * p + dl][g4 * 4 + e] * inv);
+              const int ch = dl * 4 + g4;
+              *(bf16x4*)(tb + n * 128 + ((ch ^ (n & 7)) << 4) + hh * 8) = v;
+            }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = r * 8 + (lane >> 3);
+            const u32x4 val = *(const u32x4*)(tb + row * 128 + ((ch_r ^ (row & 7)) << 4));
+            if (ok4[r]) *(u32x4*)(out + orow4[r] + p * 64 + ch_r * 8) = val;
+          }
+        }
       } else {
         const float inv = 1.f / l_tot;
         if (col_valid) {
