@@ -6,7 +6,7 @@ tables are compared bit-exactly, K/V appends by exact read-back.
 
 Every workload runs at full size in the launch configuration the benchmark
 times.  tiny, llama8b, the ICL stream batches and every hit-rate sweep point
-are checked on every request; qwen7b and large on a fixed seeded set of 16
+are checked on every request; qwen7b, large and large_prefixwarm on a fixed seeded set of 16
 requests (the extremes of cached length P and query length S, then seeded
 picks) over all heads, and large's 32 decode steps on those 16 requests at
 every step.  Each check logs its max and mean absolute error.
@@ -251,6 +251,23 @@ def test_large_decode_every_step_16_requests():
         f"mean_abs={tot / cnt:.3e}")
     _RUNS.clear()
     torch.cuda.empty_cache()
+
+
+PREFIXWARM_PARTS = 2
+
+
+@pytest.mark.parametrize("part", range(PREFIXWARM_PARTS))
+def test_large_prefixwarm_16_requests(part):
+    """The large shapes with each prompt's own 2048-token prefix cached (512 x
+    64 suffix queries over 2112 keys): 16 seeded requests, all heads."""
+    run = _full_run("large_prefixwarm")
+    assert (run.cached == 2048).all()
+    picks = _pick(run, LARGE_PICKS)
+    n = LARGE_PICKS // PREFIXWARM_PARTS
+    run.check(picks[part * n:(part + 1) * n], tag=f" picks {part * n}..{(part + 1) * n - 1}")
+    if part == PREFIXWARM_PARTS - 1:
+        _RUNS.clear()
+        torch.cuda.empty_cache()
 
 
 def test_kv_append_read_back_bit_exact():
