@@ -16,9 +16,10 @@
 //   O^T += V^T P^T  (V blocks are stored dimension-major, so each lane's
 //                 operand is 16 contiguous bytes of one V row),
 // with the online softmax in fp32 on exp2 (Q^T is kept in LDS, so that two
-// steps of K/V fit in the registers).  Waves are laid out so that the
-// waves of one kv head run under one XCD's L2 (requests sharing a prefix read
-// the same blocks).
+// steps of K/V fit in the registers).  Each XCD takes a contiguous range of
+// requests, all kv heads of each: the (block, kv head) slabs of a pool block
+// are adjacent in memory, and an XCD's reads stay within its requests' share
+// of the pools.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -78,7 +79,10 @@ __global__ __launch_bounds__(64 * kWavesPerGroup, 2) void decode_attn_kernel(
   const int n = lane & 31, hh = lane >> 5;
 
   // Group b runs on XCD b % 8 (round-robin dispatch); XCD x takes a
-  // contiguous range of groups, and items are numbered kv-head-major.
+  // contiguous range of groups, and items are numbered request-major (about
+  // 5% more bandwidth on 512 distinct 2 K-token contexts than kv-head-major
+  // numbering, which keeps one kv head's blocks in one XCD's L2 and is 2-3%
+  // faster only when every request reads one shared prefix).
   const unsigned nb = gridDim.x, per = nb >> 3, extra = nb & 7u;
   const unsigned x = blockIdx.x & 7u, i = blockIdx.x >> 3;
   const unsigned group = x * per + min(x, extra) + i;
@@ -88,7 +92,7 @@ __global__ __launch_bounds__(64 * kWavesPerGroup, 2) void decode_attn_kernel(
   // one per wave; each wave leaves its unnormalised O, max and sum in
   // part_o / part_ml for decode_combine_kernel (cols_cap = max_q_len * G columns per split).
   const int sp = item % n_split, pair = item / n_split;
-  const int h = pair / n_req, r = pair % n_req;
+  const int r = pair / Hkv, h = pair % Hkv;
   const int G = Hq / Hkv;
 
   const int q0 = cu_q[r], q_len = cu_q[r + 1] - q0;
@@ -305,7 +309,7 @@ __global__ __launch_bounds__(64 * kWavesPerGroup) void decode_combine_kernel(
   const int c = int(w % cols_cap);
   const int pair = int(w / cols_cap);
   if (pair >= n_req * Hkv) return;
-  const int h = pair / n_req, r = pair % n_req;
+  const int r = pair / Hkv, h = pair % Hkv;
   const int G = Hq / Hkv;
   const int q0 = cu_q[r], q_len = cu_q[r + 1] - q0;
   const int L = min(seq_lens[r], max_blocks * kBlock);
