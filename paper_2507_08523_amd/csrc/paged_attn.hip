@@ -179,8 +179,9 @@ constexpr int kMaxTableBlocks = 1 << 24;  // block-table width accepted (keeps t
 // Largest per-lane sum of a tile's exponentials accepted without taking the
 // tile's column max (each exponential is then at most this, 2^8).
 constexpr float kSumLimit = 256.f;
-constexpr int kQueueWords = 16;      // workspace: 8 queue counters, 1 finished-workgroup count
+constexpr int kQueueWords = 16;      // workspace: 8 queue counters, finished workgroups, drained queues
 constexpr int kDoneWord = 8;
+constexpr int kDrainedWord = 9;
 
 // s_waitcnt vmcnt(n) with the other counters left free (n < 16).
 template <int N>
@@ -268,16 +269,25 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
 
   // Item queues.  Queue x holds items [x*per + min(x, extra), ...) of
   // per + (x < extra) items; fetch() (lane 0 of wave 0 only) returns the next
-  // item, or -1 once every queue is drained.
+  // item, or -1 once every queue is drained.  The workgroup that takes the
+  // last item of a queue counts it in queue[kDrainedWord]; once the home queue
+  // is drained, that count (one round trip) tells whether any queue still
+  // holds items.  Without it, the walk over the drained queues (one contended
+  // atomic each, about 2 us) sat in front of every workgroup's last item.
   const unsigned home = xcd_id(), per = n_items >> 3, extra = n_items & 7u;
+  const unsigned nonempty = per > 0 ? 8u : extra;  // queues holding at least one item
   unsigned qsel = 0;
   auto fetch = [&]() -> int {
     while (qsel < 8u) {
       const unsigned x = (home + qsel) & 7u;
       const unsigned size = per + (x < extra ? 1u : 0u), base = x * per + min(x, extra);
       const unsigned i = __hip_atomic_fetch_add(queue + x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (i + 1 == size) __hip_atomic_fetch_add(queue + kDrainedWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (i < size) return int(base + i);
       ++qsel;
+      if (qsel == 1u &&
+          __hip_atomic_load(queue + kDrainedWord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nonempty)
+        qsel = 8u;
     }
     return -1;
   };
@@ -887,7 +897,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
     const unsigned done =
         __hip_atomic_fetch_add(queue + kDoneWord, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (done == gridDim.x - 1) {
-      for (int i = 0; i <= kDoneWord; ++i)
+      for (int i = 0; i <= kDrainedWord; ++i)
         __hip_atomic_store(queue + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
