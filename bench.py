@@ -135,6 +135,22 @@ def traffic_from_profile(workload_name: str):
     return float(fields["hbm_bytes_per_launch"]) if "hbm_bytes_per_launch" in fields else None
 
 
+def traffic_key(args) -> str:
+    """Name of the counter summary that matches this run's attention launches:
+    the workload's own for the single pass (RoPE and graph replay change
+    neither the prefill launch nor its inputs), ``<workload>_cascade`` for the
+    shared-prefix split, ``<workload>_chunk<N>`` for chunked prefill and
+    ``<workload>_nopair`` for an unrefined ICL stream."""
+    key = args.workload
+    if args.cascade:
+        key += "_cascade"
+    if args.chunk_tokens:
+        key += f"_chunk{args.chunk_tokens}"
+    if args.no_pair:
+        key += "_nopair"
+    return key
+
+
 def host_cpu():
     """The host's processor as lscpu reports it, and the CPUs this process may use."""
     info = {"nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0))}
@@ -475,7 +491,7 @@ def main():
     # the launch is bound by whichever term is larger
     t_mfma = work["flops"] / (PEAK_BF16_TFLOPS * 1e12)
     t_hbm = work["unique_bytes"] / (PEAK_HBM_GBS * 1e9)
-    traffic = None if args.prompts else traffic_from_profile(args.workload)
+    traffic = None if args.prompts else traffic_from_profile(traffic_key(args))
     if t_mfma >= t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic}

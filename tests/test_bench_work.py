@@ -87,3 +87,23 @@ def test_kernel_hash_ignores_comments_only(tmp_path, monkeypatch):
     assert bench.kernel_source_sha() == h0
     src.write_text("int f(int x) {\n  return 3 * x;\n}\n")
     assert bench.kernel_source_sha() != h0
+
+
+def test_traffic_summary_matches_the_launch_variant():
+    # a run reports measured traffic only from the summary of the same
+    # launches: the shared-prefix split, chunked steps and an unrefined ICL
+    # batch each have their own
+    import argparse
+
+    import bench
+
+    def key(**kw):
+        a = dict(workload="sweep100", cascade=False, chunk_tokens=0, no_pair=False, rope=0.0, graph=False)
+        a.update(kw)
+        return bench.traffic_key(argparse.Namespace(**a))
+
+    assert key() == "sweep100"
+    assert key(rope=5e5, graph=True) == "sweep100"
+    assert key(cascade=True) == "sweep100_cascade"
+    assert key(workload="llama8b", chunk_tokens=1024) == "llama8b_chunk1024"
+    assert key(workload="icl_llama8b", no_pair=True) == "icl_llama8b_nopair"
