@@ -431,6 +431,24 @@ def test_work_queue_workspace_reused_and_left_zeroed():
     assert int(ilpc.attn_workspace(None, side).count_nonzero()) == 0
 
 
+@pytest.mark.parametrize("n_prompts", [1, 3, 7, 9, 13])
+def test_few_items_queues_drain_and_reset(n_prompts):
+    """Launches with fewer work items than queues, or queues of uneven sizes:
+    workgroups whose own queue is drained take items from the others or stop
+    on the drained-queue count.  Every request matches the oracle, twice in a
+    row on one workspace, and the workspace is left zero-filled."""
+    run = Run(workload.scaled_spec("tiny", n_prompts))
+    b, pc, q, scale = run.batch, run.pc, run.rows["q"], run.wl.spec.scale
+    ws = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    for rep in range(2):
+        run.out.fill_(0)
+        ilpc.paged_prefill_attn(q, pc.k_pool, pc.v_pool, b.block_tables, b.cu_q, b.seq_lens, b.max_q_len,
+                                scale, run.out, ws)
+        torch.cuda.synchronize()
+        run.check(range(n_prompts), tag=f" call {rep}")
+        assert int(ws.count_nonzero()) == 0
+
+
 # -- shared-prefix split (cascade) -------------------------------------------
 
 def _cascade(run, shared_len=None):
