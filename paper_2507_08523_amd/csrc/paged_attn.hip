@@ -893,15 +893,14 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
 
   // Every queue is drained.  The last workgroup out clears the counters for
   // the next call on this workspace (no workgroup fetches any more by then).
-  // The exit count needs no fence: every queue atomic of this workgroup has
-  // been performed before it gets here (each fetch starts with a returning
-  // atomic whose value it waits for, which also covers the non-returning
-  // drained count of the fetch before it, and the last item's prologue waits
-  // for all its loads), so once the last workgroup sees the full count no
-  // queue atomic of this launch is in flight.  An acquire-release count, with
-  // its L2 write-back and invalidate at every workgroup's exit, cost 2-5% of
-  // the short launches.  The outputs are published by the end of the kernel.
+  // The exit count needs no fence.  Wave 0 (which made every queue atomic of
+  // this workgroup) first waits until all its memory operations have
+  // completed, so once the last workgroup sees the full count no queue atomic
+  // of this launch is in flight.  An acquire-release count, with its L2
+  // write-back and invalidate at every workgroup's exit, cost 2-5% of the
+  // short launches.  The outputs are published by the end of the kernel.
   if (tid == 0) {
+    wait_vmcnt<0>();
     const unsigned done =
         __hip_atomic_fetch_add(queue + kDoneWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (done == gridDim.x - 1) {
