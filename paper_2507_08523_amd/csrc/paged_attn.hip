@@ -276,7 +276,12 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   // atomic each, about 2 us) sat in front of every workgroup's last item.
   const unsigned home = xcd_id(), per = n_items >> 3, extra = n_items & 7u;
   const unsigned nonempty = per > 0 ? 8u : extra;  // queues holding at least one item
-  unsigned qsel = 0;
+  // With no more items than workgroups (grid = items), workgroup b takes
+  // item b/8 of queue b%8 (the queue of the XCD it is dispatched to in
+  // round-robin order) and nothing else: no queue atomics, no exit count,
+  // and the workspace is left untouched.  Queue x has exactly as many items
+  // as there are such workgroups.
+  unsigned qsel = 0;  // next queue to try, home first (9: the one-item-each mode)
   auto fetch = [&]() -> int {
     while (qsel < 8u) {
       const unsigned x = (home + qsel) & 7u;
@@ -312,7 +317,13 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   const bool lag = wave >= kWaves / 2;
 
   if (tid == 0) {
-    s_item[0] = fetch();
+    if (n_items <= gridDim.x) {
+      const unsigned x = blockIdx.x & 7u;
+      s_item[0] = int(x * per + min(x, extra) + (blockIdx.x >> 3));
+      qsel = 9u;  // later fetches return -1
+    } else {
+      s_item[0] = fetch();
+    }
     wait_lgkmcnt0();
   }
   __syncthreads();
@@ -899,7 +910,7 @@ __global__ __launch_bounds__(kThreads, 1) void paged_attn_kernel(
   // of this launch is in flight.  An acquire-release count, with its L2
   // write-back and invalidate at every workgroup's exit, cost 2-5% of the
   // short launches.  The outputs are published by the end of the kernel.
-  if (tid == 0) {
+  if (tid == 0 && qsel != 9u) {  // (qsel is 9 only in the one-item-each mode)
     wait_vmcnt<0>();
     const unsigned done =
         __hip_atomic_fetch_add(queue + kDoneWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
