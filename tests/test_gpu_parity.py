@@ -431,12 +431,15 @@ def test_work_queue_workspace_reused_and_left_zeroed():
     assert int(ilpc.attn_workspace(None, side).count_nonzero()) == 0
 
 
-@pytest.mark.parametrize("n_prompts", [1, 3, 7, 9, 13])
-def test_few_items_queues_drain_and_reset(n_prompts):
-    """Launches with fewer work items than queues, or queues of uneven sizes:
-    workgroups whose own queue is drained take items from the others or stop
-    on the drained-queue count.  Every request matches the oracle, twice in a
-    row on one workspace, and the workspace is left zero-filled."""
+@pytest.mark.parametrize("n_prompts", [1, 3, 7, 9, 13, 260, 300])
+def test_item_assignment_and_queue_reset(n_prompts):
+    """tiny gives one work item per request.  Up to the number of compute
+    units, every workgroup takes one item by position (fewer items than
+    queues, uneven queues); 260 and 300 items go through the queues, where
+    the workgroups left after the first round take the remaining items from
+    other XCDs' queues or stop on the drained-queue count.  Every request
+    matches the oracle, twice in a row on one workspace, and the workspace is
+    left zero-filled."""
     run = Run(workload.scaled_spec("tiny", n_prompts))
     b, pc, q, scale = run.batch, run.pc, run.rows["q"], run.wl.spec.scale
     ws = torch.zeros(64, dtype=torch.uint8, device="cuda")
