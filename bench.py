@@ -18,7 +18,7 @@ dominant kernel, the prefill attention launch, timed with HIP events on the
 stream it runs on.  ``cpu_baseline`` times the fp64 oracle on a bounded
 sample of the same workload on the host cores.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload large] [--prompts N] [--cascade] [--no-pair]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload large] [--prompts N] [--cascade | --single] [--no-pair]
 
 The default workload is ``large``: 512 prompts of 2112 tokens (16 demonstrations
 of 128 tokens + a 64-token query; 64 q / 8 kv heads, head_dim 128), whose
@@ -30,8 +30,12 @@ are reported beside them.  ``--flush-mib N`` writes N MiB of device memory
 before every step, so HBM-bound launches do not find the previous step's data
 in the caches.
 
-``--cascade`` runs the prefill attention split at the prefix every prompt of
-the batch shares (ilpc_paged_prefill_attn_cascade).
+The attention runs split at the prefix every prompt of the batch shares
+(ilpc_paged_prefill_attn_cascade) where the library's rule
+(ilpc_prefer_shared_split) expects that to be faster than the single pass --
+long shared prefixes with a short own part per prompt, as in ``sweep100`` --
+and as the single pass elsewhere; ``config.attention`` says which ran.
+``--cascade`` forces the split, ``--single`` the single pass.
 
 ``--rope BASE`` rotates the new tokens' K and Q at their positions inside the
 append (ilpc_rope_kv_append; the warm prefix is rotated the same way).
@@ -135,14 +139,14 @@ def traffic_from_profile(workload_name: str):
     return float(fields["hbm_bytes_per_launch"]) if "hbm_bytes_per_launch" in fields else None
 
 
-def traffic_key(args) -> str:
+def traffic_key(args, split: bool) -> str:
     """Name of the counter summary that matches this run's attention launches:
     the workload's own for the single pass (RoPE and graph replay change
     neither the prefill launch nor its inputs), ``<workload>_cascade`` for the
-    shared-prefix split, ``<workload>_chunk<N>`` for chunked prefill and
-    ``<workload>_nopair`` for an unrefined ICL stream."""
+    shared-prefix split (``split``), ``<workload>_chunk<N>`` for chunked
+    prefill and ``<workload>_nopair`` for an unrefined ICL stream."""
     key = args.workload
-    if args.cascade:
+    if split:
         key += "_cascade"
     if args.chunk_tokens:
         key += f"_chunk{args.chunk_tokens}"
@@ -300,7 +304,10 @@ def main():
                     help="replay the decode steps (decode workloads) and the chunked prefill steps "
                          "(--chunk-tokens) as captured HIP graphs")
     ap.add_argument("--cascade", action="store_true",
-                    help="split the prefill attention at the prefix every prompt shares")
+                    help="split the attention at the prefix every prompt shares, whatever the library's "
+                         "rule says (by default the split runs where ilpc_prefer_shared_split picks it)")
+    ap.add_argument("--single", action="store_true",
+                    help="run the single pass even where the library's rule picks the shared-prefix split")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -313,7 +320,8 @@ def main():
 
     from paper_2507_08523_amd import ilpc, workload
     from paper_2507_08523_amd.pipeline import (ChunkGraph, DecodeGraph, PagedPrefixCache, chunk_schedule,
-                                               max_blocks_of, pool_blocks_needed, rope_inv_freq, shared_prefix_len)
+                                               max_blocks_of, pool_blocks_needed, prefer_shared_split, rope_inv_freq,
+                                               shared_prefix_len)
 
     ilpc.load()
     dev = torch.device("cuda:0")
@@ -343,8 +351,8 @@ def main():
     pc = PagedPrefixCache(sp.n_kv_heads, sp.head_dim, pool_blocks_needed(wl), max_blocks_of(wl),
                           max(len(wl.prompts), len(wl.warm), 1), 20, dev)
 
-    if args.cascade and (args.rope or args.chunk_tokens):
-        print("--cascade does not combine with --rope or --chunk-tokens", file=sys.stderr)
+    if args.cascade and (args.rope or args.chunk_tokens or args.single):
+        print("--cascade does not combine with --rope, --chunk-tokens or --single", file=sys.stderr)
         sys.exit(2)
     if args.graph and (args.cascade or (args.rope and sp.decode_steps)):
         print("--graph does not combine with --cascade, nor with --rope on decode workloads", file=sys.stderr)
@@ -378,16 +386,21 @@ def main():
     out = torch.empty_like(q)
     q_rot = torch.empty_like(q) if args.rope else None
     n_chunks = len(chunk_schedule(wl.seq_lens - cached, args.chunk_tokens)) if args.chunk_tokens else 1
-    shared_len, cascade_ws = 0, None
-    if args.cascade:
-        shared_len = shared_prefix_len(cached, tables)
+    # the shared-prefix split: forced by --cascade, else where the library's
+    # rule picks it (the single pass with --single, RoPE, chunked steps or graphs)
+    shared_len = shared_prefix_len(cached, tables)
+    auto = not (args.single or args.rope or args.chunk_tokens or args.graph)
+    L = wl.seq_lens.astype(np.int32)
+    split_prefill = args.cascade or (auto and prefer_shared_split(L, shared_len))
+    split_decode = bool(dec) and (args.cascade or (auto and prefer_shared_split(L + dec, shared_len)))
+    cascade_ws = decode_ws = None
+    if split_prefill or split_decode:
         n_ws = ilpc.attn_cascade_workspace_bytes(len(wl.prompts), int((wl.seq_lens - cached).max()),
                                                  sp.n_q_heads, sp.n_kv_heads, sp.head_dim)
         cascade_ws = torch.zeros(n_ws, dtype=torch.uint8, device=dev)
         decode_ws = torch.zeros(ilpc.attn_cascade_workspace_bytes(len(wl.prompts), 1, sp.n_q_heads,
                                                                   sp.n_kv_heads, sp.head_dim),
                                 dtype=torch.uint8, device=dev)
-    L = wl.seq_lens.astype(np.int32)
     dec_in = [wl.decode_inputs(s) for s in range(dec)]
     dec_out = [torch.empty_like(d["q"]) for d in dec_in]
     dec_rot = [torch.empty_like(d["q"]) for d in dec_in] if args.rope else None
@@ -443,7 +456,7 @@ def main():
             else:
                 pc.append(b, k_new, v_new, stream)
             e[1].record(stream)
-            if args.cascade:
+            if split_prefill:
                 pc.attend_cascade(b, q, out, sp.scale, shared_len, cascade_ws, stream)
             else:
                 pc.attend(b, q_rot if args.rope else q, out, sp.scale, stream)
@@ -460,7 +473,7 @@ def main():
             else:
                 pc.append(bd, dec_in[s]["k_new"], dec_in[s]["v_new"], stream)
             dev_ev[i][s][0].record(stream)
-            if args.cascade:
+            if split_decode:
                 pc.attend_cascade(bd, qd, dec_out[s], sp.scale, shared_len, decode_ws, stream)
             else:
                 pc.attend(bd, qd, dec_out[s], sp.scale, stream)
@@ -491,7 +504,7 @@ def main():
     # the launch is bound by whichever term is larger
     t_mfma = work["flops"] / (PEAK_BF16_TFLOPS * 1e12)
     t_hbm = work["unique_bytes"] / (PEAK_HBM_GBS * 1e9)
-    traffic = None if args.prompts else traffic_from_profile(traffic_key(args))
+    traffic = None if args.prompts else traffic_from_profile(traffic_key(args, split_prefill))
     if t_mfma >= t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic}
@@ -535,7 +548,11 @@ def main():
                    "kv_heads": sp.n_kv_heads, "head_dim": sp.head_dim, "block": 16,
                    "query_tokens": work["query_tokens"], "decode_steps": dec,
                    "cached_fraction": round(float(cached.sum() / wl.seq_lens.sum()), 4),
-                   **({"cascade_shared_len": shared_len} if args.cascade else {}),
+                   "attention": {"prefill": "shared-prefix split" if split_prefill else "single pass",
+                                 **({"decode": "shared-prefix split" if split_decode else "single pass"}
+                                    if dec else {}),
+                                 "shared_len": shared_len,
+                                 "chosen_by": "--cascade" if args.cascade else ("library rule" if auto else "flags")},
                    **({"chunk_tokens": args.chunk_tokens, "chunks": n_chunks} if args.chunk_tokens else {}),
                    **({"rope_base": args.rope} if args.rope else {}),
                    **({"decode_graph": True} if dgraph is not None else {}),

@@ -442,6 +442,24 @@ int ilpc_shared_prefix_len(const int32_t* cached_len, const int32_t* block_table
                            int32_t max_blocks, int32_t* shared_len);
 
 /*
+ * Whether ilpc_paged_prefill_attn_cascade at shared_len is the faster choice
+ * for this batch than ilpc_paged_prefill_attn (host only).  The split does
+ * the same matrix-core work (section 2.1.2: every query still meets every
+ * key); it reads the shared K/V once and packs the rows of several requests
+ * into one work item, which pays where the shared keys dominate.  The rule,
+ * set from measurements on MI355X: *use = 1 when shared_len covers at least
+ * three 64-key tiles and no request has more than 128 keys past it
+ * (seq_lens[r] - shared_len <= 128), else 0.
+ *
+ * seq_lens   [host] int32 [B]  context length L_r of each request, >= shared_len
+ * shared_len as ilpc_shared_prefix_len returned it
+ * use        out: 1 or 0 (0 for B = 0)
+ * ILPC_EINVAL for NULL pointers, B < 0, shared_len < 0 or a request shorter
+ * than shared_len.
+ */
+int ilpc_prefer_shared_split(const int32_t* seq_lens, int32_t B, int32_t shared_len, int32_t* use);
+
+/*
  * Prefix-aware refinement of in-context demonstrations (section 3.2.1, with
  * its matching / modifying / reordering figure, and section 3.2.2 on the ICL
  * table).  Host only,

@@ -403,6 +403,13 @@ def rope_inv_freq(head_dim: int, base: float):
     return (base ** (-np.arange(0, head_dim, 2, dtype=np.float64) / head_dim)).astype(np.float32)
 
 
+def prefer_shared_split(seq_lens, shared_len: int) -> bool:
+    """Whether attend_cascade at shared_len should beat attend for a batch of
+    these context lengths (the library's ilpc_prefer_shared_split: at least
+    three 64-key tiles shared, at most 128 own keys per request)."""
+    return ilpc.prefer_shared_split(seq_lens, shared_len)
+
+
 def shared_prefix_len(cached_len, block_tables) -> int:
     """Keys at the front that every request of a batch shares (the library's
     ilpc_shared_prefix_len): the longest run of leading block ids equal across

@@ -97,13 +97,13 @@ def test_traffic_summary_matches_the_launch_variant():
 
     import bench
 
-    def key(**kw):
+    def key(split=False, **kw):
         a = dict(workload="sweep100", cascade=False, chunk_tokens=0, no_pair=False, rope=0.0, graph=False)
         a.update(kw)
-        return bench.traffic_key(argparse.Namespace(**a))
+        return bench.traffic_key(argparse.Namespace(**a), split)
 
     assert key() == "sweep100"
     assert key(rope=5e5, graph=True) == "sweep100"
-    assert key(cascade=True) == "sweep100_cascade"
+    assert key(split=True) == "sweep100_cascade"
     assert key(workload="llama8b", chunk_tokens=1024) == "llama8b_chunk1024"
     assert key(workload="icl_llama8b", no_pair=True) == "icl_llama8b_nopair"

@@ -101,3 +101,21 @@ def test_shared_prefix_len_cases():
     assert shared_prefix_len([32, 32], neg) == 0
     with pytest.raises(ilpc.ILPCError):
         shared_prefix_len([-16, 32], neg)
+
+
+def test_prefer_shared_split_rule():
+    # the split is chosen when the shared keys span at least three 64-key
+    # tiles and no request has more than 128 keys of its own past them
+    from paper_2507_08523_amd.ilpc import prefer_shared_split
+
+    assert prefer_shared_split([1024] * 128, 976)               # sweep100: 48 own keys
+    assert prefer_shared_split([1024 + 32] * 128, 976)          # its decode steps: 80
+    assert not prefer_shared_split([1024] * 128, 736)           # sweep75: 288 own keys
+    assert not prefer_shared_split([604] * 64, 256)             # llama8b
+    assert prefer_shared_split([192 + 128, 192], 192)           # both limits met exactly
+    assert not prefer_shared_split([192 + 129, 192], 192)       # one request past 128
+    assert not prefer_shared_split([176 + 64] * 4, 176)         # under three tiles shared
+    assert not prefer_shared_split([], 0)
+    for bad in (([100], 200), ([100], -1)):
+        with pytest.raises(ilpc.ILPCError):
+            prefer_shared_split(*bad)
