@@ -391,8 +391,9 @@ def main():
     shared_len = shared_prefix_len(cached, tables)
     auto = not (args.single or args.rope or args.chunk_tokens or args.graph)
     L = wl.seq_lens.astype(np.int32)
-    split_prefill = args.cascade or (auto and prefer_shared_split(L, shared_len))
-    split_decode = bool(dec) and (args.cascade or (auto and prefer_shared_split(L + dec, shared_len)))
+    heads = (sp.n_q_heads, sp.n_kv_heads)
+    split_prefill = args.cascade or (auto and prefer_shared_split(L, int((L - cached).max()), *heads, shared_len))
+    split_decode = bool(dec) and (args.cascade or (auto and prefer_shared_split(L + dec, 1, *heads, shared_len)))
     cascade_ws = decode_ws = None
     if split_prefill or split_decode:
         n_ws = ilpc.attn_cascade_workspace_bytes(len(wl.prompts), int((wl.seq_lens - cached).max()),

@@ -445,19 +445,23 @@ int ilpc_shared_prefix_len(const int32_t* cached_len, const int32_t* block_table
  * Whether ilpc_paged_prefill_attn_cascade at shared_len is the faster choice
  * for this batch than ilpc_paged_prefill_attn (host only).  The split does
  * the same matrix-core work (section 2.1.2: every query still meets every
- * key); it reads the shared K/V once and packs the rows of several requests
- * into one work item, which pays where the shared keys dominate.  The rule,
- * set from measurements on MI355X: *use = 1 when shared_len covers at least
- * three 64-key tiles and no request has more than 128 keys past it
- * (seq_lens[r] - shared_len <= 128), else 0.
+ * key); in one launch it reads the shared K/V once per work item and packs
+ * the rows of several requests into one item, which pays where the shared
+ * keys dominate.  The rule, set from measurements on MI355X: *use = 1 when
+ * the batch is prefill-shaped (max_q_len * Hq/Hkv > 32 query columns per
+ * request and kv head), shared_len covers at least three 64-key tiles and no
+ * request has more than 128 keys past it (seq_lens[r] - shared_len <= 128);
+ * else 0.  Decode-shaped batches keep the single pass.
  *
  * seq_lens   [host] int32 [B]  context length L_r of each request, >= shared_len
+ * max_q_len, Hq, Hkv  as for ilpc_paged_prefill_attn
  * shared_len as ilpc_shared_prefix_len returned it
  * use        out: 1 or 0 (0 for B = 0)
- * ILPC_EINVAL for NULL pointers, B < 0, shared_len < 0 or a request shorter
- * than shared_len.
+ * ILPC_EINVAL for NULL pointers, B < 0, shared_len < 0, max_q_len < 0, head
+ * counts that do not divide, or a request shorter than shared_len.
  */
-int ilpc_prefer_shared_split(const int32_t* seq_lens, int32_t B, int32_t shared_len, int32_t* use);
+int ilpc_prefer_shared_split(const int32_t* seq_lens, int32_t B, int32_t max_q_len, int32_t Hq, int32_t Hkv,
+                             int32_t shared_len, int32_t* use);
 
 /*
  * Prefix-aware refinement of in-context demonstrations (section 3.2.1, with

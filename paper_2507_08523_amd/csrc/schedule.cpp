@@ -97,17 +97,22 @@ extern "C" int ilpc_shared_prefix_len(const int32_t* cached_len, const int32_t* 
   return ILPC_OK;
 }
 
-// Measured on MI355X (prefill attention, one launch of the split against the
-// single pass): sweep100 (976 shared keys, 48 own) 9% faster, its decode
-// steps 17% faster (two launches); sweep75 (736 shared, 288 own) 3% slower,
-// llama8b and qwen7b (256 / 512 shared, 300-700 own) 9-12% slower.  The split
-// removes no matrix-core work; it pays only where the shared keys dominate
-// and each request's own keys past them fit in two 64-key tiles.
-extern "C" int ilpc_prefer_shared_split(const int32_t* seq_lens, int32_t B, int32_t shared_len, int32_t* use) {
+// Measured on MI355X against the single pass: sweep100's prefill (976 shared
+// keys, 48 own) 9% faster in one launch; sweep75 (736 shared, 288 own) 3%
+// slower; llama8b and qwen7b (256 / 512 shared, 300-700 own) 9-12% slower.
+// The split removes no matrix-core work; it pays only where the shared keys
+// dominate and each request's own keys past them fit in two 64-key tiles.
+// Decode-shaped batches (at most 32 query columns per request and kv head)
+// keep the single pass: the decode kernel reads a shared prefix from L2 per
+// request (sweep100's decode steps: 47 us single, 72 us split).
+extern "C" int ilpc_prefer_shared_split(const int32_t* seq_lens, int32_t B, int32_t max_q_len, int32_t Hq,
+                                        int32_t Hkv, int32_t shared_len, int32_t* use) {
   static const char* fn = "ilpc_prefer_shared_split";
   if (!use) return set_error(ILPC_EINVAL, "%s: use is NULL", fn);
   *use = 0;
-  if (B < 0 || shared_len < 0) return set_error(ILPC_EINVAL, "%s: B %d, shared_len %d", fn, B, shared_len);
+  if (B < 0 || shared_len < 0 || max_q_len < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0)
+    return set_error(ILPC_EINVAL, "%s: B %d, shared_len %d, max_q_len %d, heads %d/%d", fn, B, shared_len,
+                     max_q_len, Hq, Hkv);
   if (B == 0) return ILPC_OK;
   if (!seq_lens) return set_error(ILPC_EINVAL, "%s: seq_lens is NULL", fn);
   int32_t own_max = 0;
@@ -115,6 +120,7 @@ extern "C" int ilpc_prefer_shared_split(const int32_t* seq_lens, int32_t B, int3
     if (seq_lens[r] < shared_len) return set_error(ILPC_EINVAL, "%s: seq_lens[%d] < shared_len", fn, r);
     own_max = seq_lens[r] - shared_len > own_max ? seq_lens[r] - shared_len : own_max;
   }
-  *use = shared_len >= 3 * 64 && own_max <= 2 * 64 ? 1 : 0;
+  const bool prefill_shaped = int64_t(max_q_len) * (Hq / Hkv) > 32;
+  *use = prefill_shaped && shared_len >= 3 * 64 && own_max <= 2 * 64 ? 1 : 0;
   return ILPC_OK;
 }

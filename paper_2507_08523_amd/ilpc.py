@@ -56,7 +56,7 @@ _SIGS = [
     ("ilpc_chunk_schedule", _i32, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_i32),
                                    ctypes.POINTER(_i32)]),
     ("ilpc_shared_prefix_len", _i32, [_vp, _vp, _i32, _i32, ctypes.POINTER(_i32)]),
-    ("ilpc_prefer_shared_split", _i32, [_vp, _i32, _i32, ctypes.POINTER(_i32)]),
+    ("ilpc_prefer_shared_split", _i32, [_vp, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(_i32)]),
     ("ilpc_cache_create_lru", _i32, [_i32, _i32, _i32, ctypes.POINTER(_vp)]),
     ("ilpc_cache_release", _i32, [_vp, _vp, _i32, _i32]),
     ("ilpc_cache_touch", _i32, [_vp, _vp, _i32]),
@@ -281,11 +281,12 @@ def shared_prefix_len(cached_len, block_tables) -> int:
     return int(out.value)
 
 
-def prefer_shared_split(seq_lens, shared_len: int) -> bool:
+def prefer_shared_split(seq_lens, max_q_len: int, n_q_heads: int, n_kv_heads: int, shared_len: int) -> bool:
     """Whether the shared-prefix split beats the single pass (ilpc_prefer_shared_split)."""
     L = np.ascontiguousarray(seq_lens, dtype=np.int32)
     out = _i32()
-    _check(load().ilpc_prefer_shared_split(_np_ptr(L), int(L.shape[0]), int(shared_len), ctypes.byref(out)))
+    _check(load().ilpc_prefer_shared_split(_np_ptr(L), int(L.shape[0]), int(max_q_len), int(n_q_heads),
+                                           int(n_kv_heads), int(shared_len), ctypes.byref(out)))
     return bool(out.value)
 
 

@@ -403,11 +403,11 @@ def rope_inv_freq(head_dim: int, base: float):
     return (base ** (-np.arange(0, head_dim, 2, dtype=np.float64) / head_dim)).astype(np.float32)
 
 
-def prefer_shared_split(seq_lens, shared_len: int) -> bool:
-    """Whether attend_cascade at shared_len should beat attend for a batch of
-    these context lengths (the library's ilpc_prefer_shared_split: at least
-    three 64-key tiles shared, at most 128 own keys per request)."""
-    return ilpc.prefer_shared_split(seq_lens, shared_len)
+def prefer_shared_split(seq_lens, max_q_len: int, n_q_heads: int, n_kv_heads: int, shared_len: int) -> bool:
+    """Whether attend_cascade at shared_len should beat attend for this batch
+    (the library's ilpc_prefer_shared_split: prefill-shaped, at least three
+    64-key tiles shared, at most 128 own keys per request)."""
+    return ilpc.prefer_shared_split(seq_lens, max_q_len, n_q_heads, n_kv_heads, shared_len)
 
 
 def shared_prefix_len(cached_len, block_tables) -> int:

@@ -104,18 +104,24 @@ def test_shared_prefix_len_cases():
 
 
 def test_prefer_shared_split_rule():
-    # the split is chosen when the shared keys span at least three 64-key
-    # tiles and no request has more than 128 keys of its own past them
+    # the split is chosen for prefill-shaped batches whose shared keys span at
+    # least three 64-key tiles and whose requests have at most 128 keys of
+    # their own past them
     from paper_2507_08523_amd.ilpc import prefer_shared_split
 
-    assert prefer_shared_split([1024] * 128, 976)               # sweep100: 48 own keys
-    assert prefer_shared_split([1024 + 32] * 128, 976)          # its decode steps: 80
-    assert not prefer_shared_split([1024] * 128, 736)           # sweep75: 288 own keys
-    assert not prefer_shared_split([604] * 64, 256)             # llama8b
-    assert prefer_shared_split([192 + 128, 192], 192)           # both limits met exactly
-    assert not prefer_shared_split([192 + 129, 192], 192)       # one request past 128
-    assert not prefer_shared_split([176 + 64] * 4, 176)         # under three tiles shared
-    assert not prefer_shared_split([], 0)
-    for bad in (([100], 200), ([100], -1)):
+    def pick(L, shared, q=48, Hq=32, Hkv=8):
+        return prefer_shared_split(L, q, Hq, Hkv, shared)
+
+    assert pick([1024] * 128, 976)                        # sweep100: 48 own keys
+    assert not pick([1024 + 32] * 128, 976, q=1)          # its decode steps: decode-shaped
+    assert not pick([1024] * 128, 976, q=8)               # 8 rows x G 4 = 32 columns: decode-shaped
+    assert pick([1024] * 128, 976, q=9)                   # 36 columns: prefill-shaped
+    assert not pick([1024] * 128, 736)                    # sweep75: 288 own keys
+    assert not pick([604] * 64, 256)                      # llama8b
+    assert pick([192 + 128, 192], 192)                    # both limits met exactly
+    assert not pick([192 + 129, 192], 192)                # one request past 128
+    assert not pick([176 + 64] * 4, 176)                  # under three tiles shared
+    assert not pick([], 0)
+    for bad in (([100], 200, 48, 32, 8), ([100], -1, 48, 32, 8), ([100], 0, 48, 6, 4)):
         with pytest.raises(ilpc.ILPCError):
-            prefer_shared_split(*bad)
+            pick(bad[0], bad[1], q=bad[2], Hq=bad[3], Hkv=bad[4])
