@@ -55,6 +55,7 @@ class PagedPrefixCache:
         # an upload stays valid until the second upload after it.
         self._dev = [torch.empty(n, dtype=torch.int32, device=self.device) for _ in range(2)]
         self._views = {}  # (buffer, batch size) -> device views of that metadata buffer
+        self._dev_tables = [None, None]  # host copy of the block table each device buffer holds
         self._steps_host = self._steps_dev = self._steps_ev = None
 
     # -- host ---------------------------------------------------------------
@@ -94,17 +95,24 @@ class PagedPrefixCache:
             self._host_ev[i].synchronize()  # the copy that last read this buffer is done
         h, hn = self._host[i], self._host_np[i]
         nbt = B * self.max_blocks
-        hn[:nbt] = tables.reshape(-1)
+        # A block table equal to the one this device buffer already holds (the
+        # copy that wrote it is complete: its event was waited for above) is
+        # not sent again; only the lengths are.  Decode steps keep their table.
+        held = self._dev_tables[i]
+        lo = nbt if held is not None and held.shape == tables.shape and np.array_equal(held, tables) else 0
+        if lo == 0:
+            hn[:nbt] = tables.reshape(-1)
+            self._dev_tables[i] = np.array(tables, dtype=np.int32, copy=True)
         hn[nbt:nbt + B + 1] = cu_q
         hn[nbt + B + 1:nbt + 2 * B + 1] = seq_lens
         hn[nbt + 2 * B + 1:nbt + 3 * B + 1] = start_pos
         n = nbt + 3 * B + 1
         dev = self._dev[i]
         if stream == current:
-            dev[:n].copy_(h[:n], non_blocking=True)
+            dev[lo:n].copy_(h[lo:n], non_blocking=True)
         else:
             with torch.cuda.stream(stream):
-                dev[:n].copy_(h[:n], non_blocking=True)
+                dev[lo:n].copy_(h[lo:n], non_blocking=True)
         self._host_ev[i].record(stream)
         self._host_used[i] = True
         views = self._views.get((i, B))
