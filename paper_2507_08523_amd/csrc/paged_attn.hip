@@ -12,7 +12,8 @@
 //    work item is 256 query columns of one (request, kv head); a column is a
 //    (token, q head of the group) pair, so the G heads of a group share every
 //    K/V tile.  The kernel is persistent (one 8-wave workgroup per CU) and
-//    takes items from per-XCD queues.  64-key tiles (4 pool blocks) stream
+//    takes items from per-XCD queues (with no more items than CUs, one item
+//    per workgroup by position).  64-key tiles (4 pool blocks) stream
 //    through a 4-tile ring in LDS, filled by direct global-to-LDS loads
 //    issued a tile step ahead of use.  Per tile and wave:
 //      S^T = K Q^T   on v_mfma_f32_32x32x16_bf16 (a lane owns one column),
