@@ -107,3 +107,32 @@ def test_traffic_summary_matches_the_launch_variant():
     assert key(split=True) == "sweep100_cascade"
     assert key(workload="llama8b", chunk_tokens=1024) == "llama8b_chunk1024"
     assert key(workload="icl_llama8b", no_pair=True) == "icl_llama8b_nopair"
+
+
+def test_committed_summaries_name_the_current_kernel_code(monkeypatch):
+    # every counter or trace summary under profiles/ names the code hash of
+    # the kernel source it was taken on; after a code change the summaries
+    # must be taken again (bench.py then reports traffic as unmeasured)
+    import re
+
+    import bench
+
+    root = bench.ROOT
+
+    def sha(name):
+        monkeypatch.setattr(bench, "KERNEL_SRC", os.path.join(root, "paper_2507_08523_amd", "csrc", name))
+        return bench.kernel_source_sha()
+
+    current = {"paged_attn.hip": sha("paged_attn.hip"), "decode_attn.hip": sha("decode_attn.hip")}
+    prof = os.path.join(root, "profiles")
+    checked = 0
+    for fname in sorted(os.listdir(prof)):
+        text = open(os.path.join(prof, fname), encoding="utf-8").read()
+        src = "decode_attn.hip" if fname.startswith("decode_attn") else "paged_attn.hip"
+        found = re.findall(r"kernel code hash ([0-9a-f]{16})", text)
+        found += re.findall(r"^kernel_source_sha: ([0-9a-f]{16})$", text, re.M)
+        found += re.findall(r"^\w+ \| ([0-9a-f]{16}) \|", text, re.M)
+        assert found, f"{fname} names no kernel code hash"
+        assert set(found) == {current[src]}, (fname, set(found), current[src])
+        checked += 1
+    assert checked >= 20
